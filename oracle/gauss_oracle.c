@@ -24,8 +24,10 @@
  * Every function evaluates these definitions literally: a double loop, the
  * squared distance in difference form sum_d (q_d - k_d)^2, exp() from libm,
  * all arithmetic in fp64.  Alongside each result it returns the sum of the
- * absolute values of the terms (A = sum_n Phi |v_n| and its gradient
- * analogues), the scale against which a reduced-precision result is judged.
+ * absolute values of its terms, the scale against which a reduced-precision
+ * result is judged: A = sum_n Phi |v_n| for the sum, and for the q and k
+ * gradients, which are double sums over (n, c) of tau Phi g_c v_c (k - q),
+ * tau sum Phi (sum_c |g_c v_c|) |k - q|.
  *
  * Parallelism: output rows are independent; rows are split into contiguous
  * chunks over POSIX threads.  Each row is summed by one thread in index
@@ -71,6 +73,13 @@ static double dotc(const double* gm, const double* vn, int64_t C) {
   return w;
 }
 
+/* sum_c |g[m,c] v[n,c]|: the magnitude of the C terms that make up w. */
+static double absdotc(const double* gm, const double* vn, int64_t C) {
+  double w = 0.0;
+  for (int64_t c = 0; c < C; ++c) w += fabs(gm[c] * vn[c]);
+  return w;
+}
+
 /* s_m and A_m = sum_n Phi |v_n| for one query row m (Eq. 1). */
 static void fwd_row(const job_t* j, int64_t m, double* o, double* a) {
   const double* qm = j->q + m * j->D;
@@ -85,8 +94,10 @@ static void fwd_row(const job_t* j, int64_t m, double* o, double* a) {
   }
 }
 
-/* dq_m = tau sum_n Phi w (k_n - q_m) and Aq = tau sum_n Phi |w| |k_n - q_m|
- * (Sec. 3 query-gradient equation with values contracted against g_m). */
+/* dq_m = tau sum_n Phi w (k_n - q_m) (Sec. 3 query-gradient equation with
+ * values contracted against g_m).  As a double sum over (n, c) its terms are
+ * tau Phi g_mc v_nc (k_n - q_m), so the scale is
+ * Aq = tau sum_n Phi (sum_c |g_mc v_nc|) |k_n - q_m|. */
 static void dq_row(const job_t* j, int64_t m, double* o, double* a) {
   const double* qm = j->q + m * j->D;
   const double* gm = j->g + m * j->C;
@@ -95,15 +106,17 @@ static void dq_row(const job_t* j, int64_t m, double* o, double* a) {
     const double* kn = j->k + n * j->D;
     double p = phi(qm, kn, j->D, j->tau);
     double w = dotc(gm, j->v + n * j->C, j->C);
+    double wa = absdotc(gm, j->v + n * j->C, j->C);
     for (int64_t d = 0; d < j->D; ++d) {
       double diff = kn[d] - qm[d];
       o[d] += j->tau * p * w * diff;
-      a[d] += j->tau * p * fabs(w) * fabs(diff);
+      a[d] += j->tau * p * wa * fabs(diff);
     }
   }
 }
 
-/* dk_n = tau sum_m Phi w (q_m - k_n) and its absolute scale. */
+/* dk_n = tau sum_m Phi w (q_m - k_n) and its scale
+ * Ak = tau sum_m Phi (sum_c |g_mc v_nc|) |q_m - k_n|. */
 static void dk_row(const job_t* j, int64_t n, double* o, double* a) {
   const double* kn = j->k + n * j->D;
   const double* vn = j->v + n * j->C;
@@ -112,10 +125,11 @@ static void dk_row(const job_t* j, int64_t n, double* o, double* a) {
     const double* qm = j->q + m * j->D;
     double p = phi(qm, kn, j->D, j->tau);
     double w = dotc(j->g + m * j->C, vn, j->C);
+    double wa = absdotc(j->g + m * j->C, vn, j->C);
     for (int64_t d = 0; d < j->D; ++d) {
       double diff = qm[d] - kn[d];
       o[d] += j->tau * p * w * diff;
-      a[d] += j->tau * p * fabs(w) * fabs(diff);
+      a[d] += j->tau * p * wa * fabs(diff);
     }
   }
 }

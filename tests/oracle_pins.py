@@ -302,14 +302,15 @@ def pin_query_gradient_formula(orc):
 
 
 def pin_gradient_scales(orc):
-    """The absolute scales equal the sums of |terms| built from the dense matrix."""
+    """The absolute scales equal the sums of |terms| built from the dense matrix;
+    the q and k gradients are double sums over (n, c) of tau Phi g_c v_c (k - q)."""
     q, k, v, g = _problem(30, 5, 7, 3, 2)
     tau = 0.8
     Kmat = _kernel_matrix(q, k, tau).astype(np.float64)
-    W = g @ v.T                                    # w_mn
+    W = np.abs(g) @ np.abs(v).T                    # sum_c |g_mc v_nc|
     diff = k[None, :, :] - q[:, None, :]           # k_n - q_m
-    aq = tau * np.einsum("mn,mnd->md", Kmat * np.abs(W), np.abs(diff))
-    ak = tau * np.einsum("mn,mnd->nd", Kmat * np.abs(W), np.abs(diff))
+    aq = tau * np.einsum("mn,mnd->md", Kmat * W, np.abs(diff))
+    ak = tau * np.einsum("mn,mnd->nd", Kmat * W, np.abs(diff))
     av = Kmat.T @ np.abs(g)
     _close(orc.dq(q, k, v, g, tau)[1], aq, 1e-12, 1e-300, "dq scale")
     _close(orc.dk(q, k, v, g, tau)[1], ak, 1e-12, 1e-300, "dk scale")
