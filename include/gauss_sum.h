@@ -1,0 +1,136 @@
+/*
+ * gauss_sum.h -- C ABI of the MI355X (gfx950) exact Gauss-sum library.
+ *
+ * The library evaluates, for points q_1..q_M, k_1..k_N in R^D, values
+ * v_1..v_N in R^C and bandwidth tau > 0, the Gauss sum
+ *
+ *     s_m = sum_n exp(-tau/2 ||q_m - k_n||^2) v_n ,   m = 1..M
+ *
+ * (paper "Fast Gauss Sums via Flash Attention", Sec. 1, Eq. 1; the inputs and
+ * outputs follow the input/output lines of Alg. 1 and Alg. 2), and the
+ * gradients of L = sum_{m,c} dout[m,c] s[m,c] with respect to q, k and v
+ * (the query gradient is the Sec. 3 gradient equation used by MMD flows and
+ * SVGD; the key gradient is its mirror image; L is linear in v).
+ *
+ * Memory and ownership
+ *   - Every data pointer is a DEVICE pointer owned by the caller.  All arrays
+ *     are dense, row-major and contiguous: q is M x D, k is N x D, v is N x C,
+ *     dout and out are M x C, dq is M x D, dk is N x D, dv is N x C.
+ *   - Each pointer must be aligned to its element size; the workspace to 256
+ *     bytes.
+ *   - q and k may be the same array (M == N), as in MMD and SVGD.  Outputs
+ *     must not overlap any input, the workspace or each other.
+ *   - The library allocates nothing.  The caller provides a device workspace
+ *     of at least the size returned by the *_workspace_size query; its
+ *     contents on entry are ignored and on exit undefined.
+ *
+ * Execution
+ *   - All work is enqueued on `stream` (NULL = the default stream) and runs
+ *     asynchronously; the returned status covers argument validation and
+ *     kernel launches only.  No call synchronises with the device.
+ *   - Arguments are validated before anything is enqueued: on any error
+ *     status no kernel has been launched and no output was touched.
+ *   - Inputs must stay valid until the enqueued work completes.  Calls on
+ *     different streams may overlap only if their workspaces are disjoint.
+ *   - Results are deterministic: the same inputs give bitwise identical
+ *     outputs on every run (fixed summation order, no atomics on data).
+ *   - NaN or Inf inside the data propagate; they are not checked.
+ *
+ * Precision
+ *   - q, k: fp16 or bf16.  v, dout: fp32, fp16 or bf16.  Outputs: fp32.
+ *   - Dot products q.k use fp16/bf16 matrix cores with fp32 accumulation; the
+ *     exponent tau*q.k - tau/2||q||^2 - tau/2||k||^2 is formed in fp32 and
+ *     clamped at <= 0; kernel values and values are contracted in fp16 with
+ *     fp32 accumulation after exact power-of-two scaling.  Each result is
+ *     within 2e-3 (fp16 q,k) or 5e-3 (bf16 q,k) of sum_n Phi |v_n| per element
+ *     of the exact value (and the analogous sums of |terms| for gradients).
+ */
+#ifndef GAUSS_SUM_H
+#define GAUSS_SUM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GAUSS_SUM_ABI_VERSION 1
+#define GAUSS_SUM_MAX_DIM 256 /* largest D and C accepted */
+
+typedef enum { GS_F32 = 0, GS_F16 = 1, GS_BF16 = 2 } gs_dtype;
+
+typedef enum {
+  GS_SUCCESS = 0,
+  GS_ERR_NULL_POINTER = 1, /* a required pointer is NULL, or no output requested */
+  GS_ERR_BAD_SHAPE = 2,    /* M < 0, N < 0, D or C outside [1, 256] */
+  GS_ERR_BAD_TAU = 3,      /* tau not finite or not > 0 (Eq. 1 needs tau > 0) */
+  GS_ERR_UNSUPPORTED = 4,  /* dtype combination not supported */
+  GS_ERR_MISALIGNED = 5,   /* pointer not aligned as documented above */
+  GS_ERR_WORKSPACE = 6,    /* workspace NULL or smaller than required */
+  GS_ERR_HIP = 7,          /* a HIP runtime call or kernel launch failed */
+  GS_ERR_INTERNAL = 8,     /* unexpected internal failure */
+  GS_ERR_ALIAS = 9         /* an output overlaps an input or another output */
+} gs_status;
+
+/* Problem description.  qk_dtype: GS_F16 or GS_BF16 (both q and k).
+ * v_dtype: GS_F32, GS_F16 or GS_BF16. */
+typedef struct {
+  int64_t M, N, D, C;
+  gs_dtype qk_dtype;
+  gs_dtype v_dtype;
+} gs_problem;
+
+/* Bytes of device workspace gauss_sum_fwd needs for problem p (0 if p is
+ * invalid or NULL). */
+size_t gauss_sum_fwd_workspace_size(const gs_problem* p);
+
+/* Bytes of device workspace gauss_sum_bwd needs for problem p and the
+ * requested gradients (flags nonzero = requested; 0 if p is invalid). */
+size_t gauss_sum_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv);
+
+/* Forward, Eq. 1: out[m,c] = s_m[c] for m < M, c < C (fp32, overwritten).
+ * M == 0 is a no-op; N == 0 writes zeros. */
+gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
+                        float* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Backward: for L = sum_{m,c} dout[m,c] s[m,c] (dout: M x C of dout_dtype,
+ * GS_F32, GS_F16 or GS_BF16) writes
+ *   dq[m,:] = tau sum_n Phi_mn <dout_m, v_n> (k_n - q_m)   (Sec. 3 gradient)
+ *   dk[n,:] = tau sum_m Phi_mn <dout_m, v_n> (q_m - k_n)
+ *   dv[n,:] =     sum_m Phi_mn dout_m
+ * Any of dq, dk, dv may be NULL (not computed); at least one must be given.
+ * Outputs are fp32 and overwritten. */
+gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
+                        const void* dout, gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Static, never-NULL description of a status code. */
+const char* gauss_sum_status_string(gs_status s);
+
+/* GAUSS_SUM_ABI_VERSION of the built library. */
+int gauss_sum_abi_version(void);
+
+/* Kernel timing hook for benchmarks and profiling; not needed to compute.
+ * gauss_sum_profile_start(capacity, kind) creates 2*capacity HIP events on
+ * the current device; afterwards each launch of a main kernel selected by
+ * `kind` (1 = forward-type kernels, 2 = gradient-type kernels, 3 = both),
+ * across all following calls, is bracketed by a pair of events recorded on
+ * the call's stream, until capacity launches are recorded.
+ * gauss_sum_profile_stop(ms, max) waits for those events, writes up to `max`
+ * per-launch durations in milliseconds (host array) and returns how many
+ * launches were recorded (negative on a HIP error); it releases the events.
+ * Status: GS_ERR_BAD_SHAPE for capacity < 1 or kind outside 1..3, GS_ERR_HIP
+ * if events cannot be created.  The hook is process-global and not
+ * thread-safe: use it from one thread while no other thread calls the
+ * library. */
+gs_status gauss_sum_profile_start(int capacity, int kind);
+int gauss_sum_profile_stop(float* ms, int max);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GAUSS_SUM_H */

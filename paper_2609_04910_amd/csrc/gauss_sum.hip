@@ -1,0 +1,635 @@
+// gauss_sum.hip -- C ABI of the gfx950 Gauss-sum library: validation, launch
+// planning, workspace carving and kernel dispatch.  Declarations and the
+// contract of every entry point are in include/gauss_sum.h.
+#include "../../include/gauss_sum.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+
+#include "gs_common.h"
+#include "gs_kernels.h"
+#include "gs_prep.h"
+
+namespace gs {
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kRowBoundSamples = 64;
+constexpr int kTargetBlocks = 1024;   // workgroups per pass before splitting over keys
+constexpr int kMinStepsPerSplit = 4;  // 128 keys
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+inline int pow2_chunks(int64_t width, int unit, int max_chunks) {
+  int c = 1;
+  while (c * unit < width && c < max_chunks) c *= 2;
+  return c;
+}
+
+// Shape parameters of the tiles (see gs_common.h for the layouts).
+struct Dims {
+  int DP;  // 32-wide chunks of D (1, 2, 4, 8): RT width W = 32 DP, KS rows = 32 DP
+  int CW;  // 32-wide chunks of C (1, 2, 4, 8): RT width of values = 32 CW
+  int CT;  // 16-row tiles of C (1, 2, 4, 8, 16): KS rows of values = 16 CT
+  int W() const { return 32 * DP; }
+  int Wv() const { return 32 * CW; }
+  int Rv() const { return 16 * CT; }
+};
+
+inline Dims dims_of(int64_t D, int64_t C) {
+  Dims d;
+  d.DP = pow2_chunks(D, 32, 8);
+  d.CW = pow2_chunks(C, 32, 8);
+  d.CT = pow2_chunks(C, 16, 16);
+  return d;
+}
+
+// Query tiles per wave: the largest of 4, 2, 1 whose kernel (as compiled for
+// gfx950) needs at most 256 registers per lane, i.e. keeps two waves per SIMD;
+// the D = 256 gradient kernel needs ~280 at one tile and runs one wave per SIMD.
+constexpr int fwd_qt(int DP, int CT) {
+  return CT >= 16 ? 1 : CT == 8 ? 2 : (DP == 8 && CT > 1) ? 2 : 4;
+}
+constexpr int dq_qt(int DP, int CW) {
+  return DP >= 4 ? 1 : DP == 2 ? 2 : CW >= 4 ? 2 : 4;
+}
+
+// ------------------------------------------------------------ dispatch tables
+
+template <typename T, int DP, int CT, int QT>
+void launch_fwd_q(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const float* Lq,
+                  const uint4* ks, const float* nhk, const uint4* vt, const uint32_t* vslot,
+                  float tau2, int64_t M, int C, int steps, int sps, float* out, int64_t pstride) {
+  hipLaunchKernelGGL((k_fwd<T, DP, CT, QT>), grid, dim3(kBlockThreads), 0, st, qs, nhq, Lq, ks, nhk,
+                     vt, vslot, tau2, M, C, steps, sps, out, pstride);
+}
+
+using FwdFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const float*, const uint4*,
+                       const float*, const uint4*, const uint32_t*, float, int64_t, int, int, int,
+                       float*, int64_t);
+
+template <typename T, int DP, int CT>
+constexpr FwdFn fwd_entry() {
+  return &launch_fwd_q<T, DP, CT, fwd_qt(DP, CT)>;
+}
+
+template <typename T, int DP>
+FwdFn fwd_by_ct(int CT) {
+  switch (CT) {
+    case 1: return fwd_entry<T, DP, 1>();
+    case 2: return fwd_entry<T, DP, 2>();
+    case 4: return fwd_entry<T, DP, 4>();
+    case 8: return fwd_entry<T, DP, 8>();
+    case 16: return fwd_entry<T, DP, 16>();
+  }
+  return nullptr;
+}
+
+template <typename T>
+FwdFn fwd_fn(int DP, int CT) {
+  switch (DP) {
+    case 1: return fwd_by_ct<T, 1>(CT);
+    case 2: return fwd_by_ct<T, 2>(CT);
+    case 4: return fwd_by_ct<T, 4>(CT);
+    case 8: return fwd_by_ct<T, 8>(CT);
+  }
+  return nullptr;
+}
+
+template <typename T, int DP, int CW, int QT>
+void launch_dq_q(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const float* Lq,
+                 const uint4* ks, const float* nhk, const uint4* kt, const uint32_t* kslot,
+                 const uint4* vs, const uint32_t* vslot, const uint4* gsr, const uint32_t* gslot,
+                 float tau2, float tau, int64_t M, int D, int steps, int sps, float* out,
+                 int64_t pstride) {
+  hipLaunchKernelGGL((k_dq<T, DP, CW, QT>), grid, dim3(kBlockThreads), 0, st, qs, nhq, Lq, ks, nhk,
+                     kt, kslot, vs, vslot, gsr, gslot, tau2, tau, M, D, steps, sps, out, pstride);
+}
+
+using DqFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const float*, const uint4*,
+                      const float*, const uint4*, const uint32_t*, const uint4*, const uint32_t*,
+                      const uint4*, const uint32_t*, float, float, int64_t, int, int, int, float*,
+                      int64_t);
+
+template <typename T, int DP, int CW>
+constexpr DqFn dq_entry() {
+  return &launch_dq_q<T, DP, CW, dq_qt(DP, CW)>;
+}
+
+template <typename T, int DP>
+DqFn dq_by_cw(int CW) {
+  switch (CW) {
+    case 1: return dq_entry<T, DP, 1>();
+    case 2: return dq_entry<T, DP, 2>();
+    case 4: return dq_entry<T, DP, 4>();
+    case 8: return dq_entry<T, DP, 8>();
+  }
+  return nullptr;
+}
+
+template <typename T>
+DqFn dq_fn(int DP, int CW) {
+  switch (DP) {
+    case 1: return dq_by_cw<T, 1>(CW);
+    case 2: return dq_by_cw<T, 2>(CW);
+    case 4: return dq_by_cw<T, 4>(CW);
+    case 8: return dq_by_cw<T, 8>(CW);
+  }
+  return nullptr;
+}
+
+// ------------------------------------------------------------ workspace plan
+
+struct Carver {
+  size_t off = 0;
+  char* base = nullptr;
+  template <typename P>
+  P* take(size_t bytes) {
+    size_t at = off;
+    off = round_up((int64_t)(off + bytes), kAlign);
+    return base ? reinterpret_cast<P*>(base + at) : nullptr;
+  }
+};
+
+struct Side {  // one point set with the arrays derived from it
+  uint16_t* rt = nullptr;  // RT copy (input dtype)
+  float* nh = nullptr;     // -||x||^2/2
+  float* L = nullptr;      // sampled row bound (as queries against the other set)
+  uint16_t* ks = nullptr;  // KS fp16 copy (operand of sum_n P k_n)
+};
+
+struct Vals {  // one value set (v or dout)
+  uint16_t* rt = nullptr;
+  uint16_t* ks = nullptr;
+};
+
+struct Plan {
+  Dims dm;
+  int64_t Mp = 0, Np = 0;
+  bool alias = false;  // q and k are the same array
+  uint32_t* slots = nullptr;  // [0] |v| max, [1] |dout| max, [2] |q| max, [3] |k| max
+  Side q, k;
+  Vals v, g;
+  float* part = nullptr;
+  size_t part_bytes = 0;
+  size_t total = 0;
+};
+
+struct PassShape {
+  int QT, blocks, splits, sps, steps;
+};
+
+PassShape pass_shape(int64_t rows, int64_t keys, int QT) {
+  PassShape ps;
+  ps.QT = QT;
+  ps.blocks = (int)ceil_div(rows, 64 * QT);
+  ps.steps = (int)ceil_div(keys, kStep);
+  int want = (int)std::max<int64_t>(1, ceil_div(kTargetBlocks, std::max(1, ps.blocks)));
+  int cap = std::max(1, ps.steps / kMinStepsPerSplit);
+  int splits = std::max(1, std::min(want, cap));
+  ps.sps = (int)ceil_div(ps.steps, splits);
+  ps.splits = ps.steps ? (int)ceil_div(ps.steps, ps.sps) : 1;
+  return ps;
+}
+
+struct Want {
+  bool fwd = false, dq = false, dk = false, dv = false;
+};
+
+// Lays out every buffer the requested passes need; with ws == nullptr only
+// computes the size.
+void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& pl) {
+  pl.dm = dims_of(p.D, p.C);
+  pl.Mp = round_up(std::max<int64_t>(p.M, 1), kRowPad);
+  pl.Np = round_up(std::max<int64_t>(p.N, 1), kRowPad);
+  pl.alias = alias;
+  const int W = pl.dm.W(), Wv = pl.dm.Wv(), Rv = pl.dm.Rv();
+  Carver cv;
+  cv.base = static_cast<char*>(ws);
+  pl.slots = cv.take<uint32_t>(64);
+  const bool need_k_ks = w.dq, need_q_ks = w.dk;
+  const bool need_Lk = w.dk || w.dv;
+  pl.q.rt = cv.take<uint16_t>(pl.Mp * W * 2);
+  pl.q.nh = cv.take<float>(pl.Mp * 4);
+  pl.q.L = cv.take<float>(pl.Mp * 4);
+  if (need_q_ks || (alias && need_k_ks)) pl.q.ks = cv.take<uint16_t>(pl.Mp * W * 2);
+  if (alias) {
+    pl.k = pl.q;
+  } else {
+    pl.k.rt = cv.take<uint16_t>(pl.Np * W * 2);
+    pl.k.nh = cv.take<float>(pl.Np * 4);
+    if (need_Lk) pl.k.L = cv.take<float>(pl.Np * 4);
+    if (need_k_ks) pl.k.ks = cv.take<uint16_t>(pl.Np * W * 2);
+  }
+  if (w.dq || w.dk) pl.v.rt = cv.take<uint16_t>(pl.Np * Wv * 2);
+  if (w.fwd) pl.v.ks = cv.take<uint16_t>(pl.Np * Rv * 2);
+  if (w.dq || w.dk) pl.g.rt = cv.take<uint16_t>(pl.Mp * Wv * 2);
+  if (w.dv) pl.g.ks = cv.take<uint16_t>(pl.Mp * Rv * 2);
+
+  // Partial-sum buffer for split passes (reused by every pass in turn).
+  size_t part = 0;
+  auto consider = [&](int64_t rows, int64_t keys, int QT, int64_t width) {
+    PassShape ps = pass_shape(rows, keys, QT);
+    if (ps.splits > 1) part = std::max(part, (size_t)ps.splits * rows * width * 4);
+  };
+  const int qf = fwd_qt(pl.dm.DP, pl.dm.CT), qd = dq_qt(pl.dm.DP, pl.dm.CW);
+  if (w.fwd) consider(p.M, p.N, qf, p.C);
+  if (w.dq) consider(p.M, p.N, qd, p.D);
+  if (w.dk) consider(p.N, p.M, qd, p.D);
+  if (w.dv) consider(p.N, p.M, qf, p.C);
+  pl.part_bytes = part;
+  pl.part = part ? cv.take<float>(part) : nullptr;
+  pl.total = cv.off;
+}
+
+// ------------------------------------------------------------ timing hook
+
+struct Profiler {
+  hipEvent_t* ev = nullptr;
+  int capacity = 0, used = 0, kind = 0;
+};
+Profiler g_prof;
+
+enum { kKindFwd = 1, kKindGrad = 2 };
+
+inline void prof_before(int kind, hipStream_t st) {
+  if (g_prof.ev && (g_prof.kind & kind) && g_prof.used < g_prof.capacity)
+    (void)hipEventRecord(g_prof.ev[2 * g_prof.used], st);
+}
+inline void prof_after(int kind, hipStream_t st) {
+  if (g_prof.ev && (g_prof.kind & kind) && g_prof.used < g_prof.capacity) {
+    (void)hipEventRecord(g_prof.ev[2 * g_prof.used + 1], st);
+    ++g_prof.used;
+  }
+}
+
+void prof_release() {
+  if (!g_prof.ev) return;
+  for (int i = 0; i < 2 * g_prof.capacity; ++i)
+    if (g_prof.ev[i]) (void)hipEventDestroy(g_prof.ev[i]);
+  delete[] g_prof.ev;
+  g_prof = Profiler();
+}
+
+// ------------------------------------------------------------ launches
+
+inline unsigned grid1(int64_t n, int threads = 256) {
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(n, threads), 1 << 20));
+}
+
+struct Ctx {
+  hipStream_t st;
+  const gs_problem* p;
+  Plan* pl;
+  float tau, tau2;
+};
+
+void prep_points(const Ctx& c, const void* x, int64_t n, int64_t n_pad, Side& s, uint32_t* slot,
+                 bool ks_copy) {
+  const gs_problem& p = *c.p;
+  const int W = c.pl->dm.W();
+  const uint16_t* x16 = static_cast<const uint16_t*>(x);
+  hipLaunchKernelGGL(k_points_rt, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D, n_pad,
+                     W, s.rt);
+  if (p.qk_dtype == GS_F16)
+    hipLaunchKernelGGL(k_points_norm<F16>, dim3(grid1(n_pad)), dim3(256), 0, c.st, x16, n, (int)p.D,
+                       n_pad, s.nh);
+  else
+    hipLaunchKernelGGL(k_points_norm<BF16>, dim3(grid1(n_pad)), dim3(256), 0, c.st, x16, n, (int)p.D,
+                       n_pad, s.nh);
+  if (ks_copy) {
+    if (p.qk_dtype == GS_F16) {
+      hipLaunchKernelGGL(k_points_ks<F16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n,
+                         (int)p.D, n_pad, W, (const uint32_t*)nullptr, s.ks);
+    } else {
+      hipLaunchKernelGGL(k_absmax, dim3(grid1(n * p.D, 256)), dim3(256), 0, c.st, x, n * p.D, 2,
+                         slot);
+      hipLaunchKernelGGL(k_points_ks<BF16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n,
+                         (int)p.D, n_pad, W, (const uint32_t*)slot, s.ks);
+    }
+  }
+}
+
+void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t n, int64_t n_pad, Vals& s,
+                 uint32_t* slot) {
+  const gs_problem& p = *c.p;
+  const int Wv = c.pl->dm.Wv(), Rv = c.pl->dm.Rv();
+  if (n > 0)
+    hipLaunchKernelGGL(k_absmax, dim3(grid1(n * p.C, 256)), dim3(256), 0, c.st, x, n * p.C, (int)dt,
+                       slot);
+  if (s.rt)
+    hipLaunchKernelGGL(k_values_rt, dim3(grid1(n_pad * Wv)), dim3(256), 0, c.st, x, (int)dt, n,
+                       (int)p.C, n_pad, Wv, (const uint32_t*)slot, s.rt);
+  if (s.ks)
+    hipLaunchKernelGGL(k_values_ks, dim3(grid1(n_pad * Rv)), dim3(256), 0, c.st, x, (int)dt, n,
+                       (int)p.C, n_pad, Rv, (const uint32_t*)slot, s.ks);
+}
+
+void row_bound(const Ctx& c, const Side& qside, int64_t nq, int64_t nq_pad, const Side& kside,
+               int64_t nk) {
+  const gs_problem& p = *c.p;
+  const int W = c.pl->dm.W();
+  const int samples = (int)std::min<int64_t>(kRowBoundSamples, std::max<int64_t>(nk, 1));
+  if (p.qk_dtype == GS_F16)
+    hipLaunchKernelGGL(k_row_bound<F16>, dim3(grid1(nq_pad)), dim3(256), 0, c.st, qside.rt, qside.nh,
+                       nq, nq_pad, kside.rt, kside.nh, nk, (int)p.D, W, c.tau2, samples, qside.L);
+  else
+    hipLaunchKernelGGL(k_row_bound<BF16>, dim3(grid1(nq_pad)), dim3(256), 0, c.st, qside.rt,
+                       qside.nh, nq, nq_pad, kside.rt, kside.nh, nk, (int)p.D, W, c.tau2, samples,
+                       qside.L);
+}
+
+void combine(const Ctx& c, const PassShape& ps, int64_t count, float* out) {
+  if (ps.splits > 1)
+    hipLaunchKernelGGL(k_combine, dim3(grid1(count)), dim3(256), 0, c.st, (const float*)c.pl->part,
+                       ps.splits, count, out);
+}
+
+// Forward-type pass: out[m, :] = sum_n Phi(x_m, y_n) val_n for x = qside rows.
+void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk,
+              const uint16_t* vks, const uint32_t* vslot, float* out) {
+  const gs_problem& p = *c.p;
+  const Dims& dm = c.pl->dm;
+  PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT));
+  FwdFn fn = p.qk_dtype == GS_F16 ? fwd_fn<F16>(dm.DP, dm.CT) : fwd_fn<BF16>(dm.DP, dm.CT);
+  float* dst = ps.splits > 1 ? c.pl->part : out;
+  prof_before(kKindFwd, c.st);
+  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, qs.L, (const uint4*)ks.rt, ks.nh,
+     (const uint4*)vks, vslot, c.tau2, nq, (int)p.C, ps.steps, ps.sps, dst,
+     ps.splits > 1 ? nq * p.C : 0);
+  prof_after(kKindFwd, c.st);
+  combine(c, ps, nq * p.C, out);
+}
+
+// dq-type pass: out[m, :] = tau sum_n Phi(x_m, y_n) <gx_m, vy_n> (y_n - x_m).
+void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const uint32_t* kslot,
+             const uint16_t* vrt, const uint32_t* vslot, const uint16_t* grt, const uint32_t* gslot,
+             float* out) {
+  const gs_problem& p = *c.p;
+  const Dims& dm = c.pl->dm;
+  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, dm.CW));
+  DqFn fn = p.qk_dtype == GS_F16 ? dq_fn<F16>(dm.DP, dm.CW) : dq_fn<BF16>(dm.DP, dm.CW);
+  float* dst = ps.splits > 1 ? c.pl->part : out;
+  prof_before(kKindGrad, c.st);
+  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, qs.L, (const uint4*)ks.rt, ks.nh,
+     (const uint4*)ks.ks, p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot,
+     (const uint4*)grt, gslot, c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst,
+     ps.splits > 1 ? nq * p.D : 0);
+  prof_after(kKindGrad, c.st);
+  combine(c, ps, nq * p.D, out);
+}
+
+void fill_zero(hipStream_t st, float* p, int64_t n) {
+  if (p && n > 0) hipLaunchKernelGGL(k_fill_f32, dim3(grid1(n)), dim3(256), 0, st, p, n, 0.0f);
+}
+
+// ------------------------------------------------------------ validation
+
+size_t dsize(gs_dtype t) { return t == GS_F32 ? 4 : 2; }
+
+bool valid_dtype(gs_dtype t) { return t == GS_F32 || t == GS_F16 || t == GS_BF16; }
+
+gs_status check_problem(const gs_problem* p) {
+  if (!p) return GS_ERR_NULL_POINTER;
+  if (p->M < 0 || p->N < 0 || p->D < 1 || p->D > GAUSS_SUM_MAX_DIM || p->C < 1 ||
+      p->C > GAUSS_SUM_MAX_DIM)
+    return GS_ERR_BAD_SHAPE;
+  if (p->M > (int64_t(1) << 36) || p->N > (int64_t(1) << 36)) return GS_ERR_BAD_SHAPE;
+  if (p->qk_dtype != GS_F16 && p->qk_dtype != GS_BF16) return GS_ERR_UNSUPPORTED;
+  if (!valid_dtype(p->v_dtype)) return GS_ERR_UNSUPPORTED;
+  return GS_SUCCESS;
+}
+
+gs_status check_tau(float tau) {
+  if (!(tau > 0.0f) || !std::isfinite(tau)) return GS_ERR_BAD_TAU;
+  return GS_SUCCESS;
+}
+
+bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
+
+struct Range {
+  uintptr_t lo, hi;
+};
+Range range_of(const void* ptr, int64_t bytes) {
+  uintptr_t a = reinterpret_cast<uintptr_t>(ptr);
+  return Range{a, a + (uintptr_t)std::max<int64_t>(bytes, 0)};
+}
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi && a.hi > a.lo && b.hi > b.lo; }
+
+gs_status check_workspace(void* ws, size_t have, size_t need) {
+  if (need == 0) return GS_SUCCESS;
+  if (!ws) return GS_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return GS_ERR_MISALIGNED;
+  if (have < need) return GS_ERR_WORKSPACE;
+  return GS_SUCCESS;
+}
+
+gs_status launch_status() {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? GS_SUCCESS : GS_ERR_HIP;
+}
+
+}  // namespace
+}  // namespace gs
+
+using namespace gs;
+
+extern "C" {
+
+int gauss_sum_abi_version(void) { return GAUSS_SUM_ABI_VERSION; }
+
+const char* gauss_sum_status_string(gs_status s) {
+  switch (s) {
+    case GS_SUCCESS: return "success";
+    case GS_ERR_NULL_POINTER: return "a required pointer is NULL or no output was requested";
+    case GS_ERR_BAD_SHAPE: return "bad shape: need M, N >= 0 and 1 <= D, C <= 256";
+    case GS_ERR_BAD_TAU: return "tau must be finite and > 0";
+    case GS_ERR_UNSUPPORTED: return "unsupported dtype combination";
+    case GS_ERR_MISALIGNED: return "pointer not aligned (elements to their size, workspace to 256 bytes)";
+    case GS_ERR_WORKSPACE: return "workspace missing or smaller than required";
+    case GS_ERR_HIP: return "HIP runtime error";
+    case GS_ERR_INTERNAL: return "internal error";
+    case GS_ERR_ALIAS: return "an output overlaps an input or another output";
+  }
+  return "unknown status";
+}
+
+gs_status gauss_sum_profile_start(int capacity, int kind) {
+  if (capacity < 1 || kind < 1 || kind > 3) return GS_ERR_BAD_SHAPE;
+  prof_release();
+  g_prof.ev = new (std::nothrow) hipEvent_t[2 * (size_t)capacity]();
+  if (!g_prof.ev) return GS_ERR_INTERNAL;
+  g_prof.capacity = capacity;
+  g_prof.kind = kind;
+  for (int i = 0; i < 2 * capacity; ++i) {
+    if (hipEventCreate(&g_prof.ev[i]) != hipSuccess) {
+      prof_release();
+      return GS_ERR_HIP;
+    }
+  }
+  return GS_SUCCESS;
+}
+
+int gauss_sum_profile_stop(float* ms, int max) {
+  if (!g_prof.ev) return 0;
+  int n = g_prof.used, rc = n;
+  for (int i = 0; i < n; ++i) {
+    if (hipEventSynchronize(g_prof.ev[2 * i + 1]) != hipSuccess) { rc = -1; break; }
+    float t = 0.0f;
+    if (hipEventElapsedTime(&t, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]) != hipSuccess) {
+      rc = -1;
+      break;
+    }
+    if (ms && i < max) ms[i] = t;
+  }
+  prof_release();
+  return rc;
+}
+
+size_t gauss_sum_fwd_workspace_size(const gs_problem* p) {
+  if (check_problem(p) != GS_SUCCESS) return 0;
+  if (p->M == 0 || p->N == 0) return 0;
+  Want w;
+  w.fwd = true;
+  Plan pl;
+  make_plan(*p, w, false, nullptr, pl);
+  return pl.total;
+}
+
+size_t gauss_sum_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv) {
+  if (check_problem(p) != GS_SUCCESS) return 0;
+  if (p->M == 0 || p->N == 0) return 0;
+  Want w;
+  w.dq = want_dq != 0;
+  w.dk = want_dk != 0;
+  w.dv = want_dv != 0;
+  if (!w.dq && !w.dk && !w.dv) return 0;
+  Plan pl;
+  make_plan(*p, w, false, nullptr, pl);
+  return pl.total;
+}
+
+gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
+                        float* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  try {
+    gs_status st = check_problem(p);
+    if (st != GS_SUCCESS) return st;
+    if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+    const int64_t M = p->M, N = p->N, D = p->D, C = p->C;
+    if (M == 0) return GS_SUCCESS;
+    if (!out || !q || (N > 0 && (!k || !v))) return GS_ERR_NULL_POINTER;
+    if (!aligned(q, 2) || (N > 0 && (!aligned(k, 2) || !aligned(v, dsize(p->v_dtype)))) ||
+        !aligned(out, 4))
+      return GS_ERR_MISALIGNED;
+    Range ro = range_of(out, M * C * 4);
+    if (overlap(ro, range_of(q, M * D * 2)) ||
+        (N > 0 && (overlap(ro, range_of(k, N * D * 2)) ||
+                   overlap(ro, range_of(v, N * C * (int64_t)dsize(p->v_dtype))))))
+      return GS_ERR_ALIAS;
+    if (N == 0) {
+      fill_zero(stream, out, M * C);
+      return launch_status();
+    }
+    const bool alias = (q == k) && (M == N);
+    Want w;
+    w.fwd = true;
+    Plan pl;
+    make_plan(*p, w, alias, nullptr, pl);
+    if ((st = check_workspace(workspace, workspace_bytes, pl.total)) != GS_SUCCESS) return st;
+    Range rw = range_of(workspace, (int64_t)pl.total);
+    if (overlap(ro, rw) || overlap(rw, range_of(q, M * D * 2)) || overlap(rw, range_of(k, N * D * 2)) ||
+        overlap(rw, range_of(v, N * C * (int64_t)dsize(p->v_dtype))))
+      return GS_ERR_ALIAS;
+    make_plan(*p, w, alias, workspace, pl);
+
+    Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
+    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
+    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, false);
+    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, false);
+    prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
+    row_bound(c, pl.q, M, pl.Mp, pl.k, N);
+    pass_fwd(c, pl.q, M, pl.k, N, pl.v.ks, pl.slots + 0, out);
+    return launch_status();
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
+
+gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
+                        const void* dout, gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  try {
+    gs_status st = check_problem(p);
+    if (st != GS_SUCCESS) return st;
+    if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+    if (!valid_dtype(dout_dtype)) return GS_ERR_UNSUPPORTED;
+    if (!dq && !dk && !dv) return GS_ERR_NULL_POINTER;
+    const int64_t M = p->M, N = p->N, D = p->D, C = p->C;
+    if ((M > 0 && (!q || !dout)) || (N > 0 && (!k || !v))) return GS_ERR_NULL_POINTER;
+    const size_t vs = dsize(p->v_dtype), gsz = dsize(dout_dtype);
+    if ((M > 0 && (!aligned(q, 2) || !aligned(dout, gsz))) ||
+        (N > 0 && (!aligned(k, 2) || !aligned(v, vs))) || (dq && !aligned(dq, 4)) ||
+        (dk && !aligned(dk, 4)) || (dv && !aligned(dv, 4)))
+      return GS_ERR_MISALIGNED;
+    Range in[4] = {range_of(q, M * D * 2), range_of(k, N * D * 2), range_of(v, N * C * (int64_t)vs),
+                   range_of(dout, M * C * (int64_t)gsz)};
+    Range outs[3] = {range_of(dq, dq ? M * D * 4 : 0), range_of(dk, dk ? N * D * 4 : 0),
+                     range_of(dv, dv ? N * C * 4 : 0)};
+    for (int a = 0; a < 3; ++a) {
+      for (int b = 0; b < 4; ++b)
+        if (overlap(outs[a], in[b])) return GS_ERR_ALIAS;
+      for (int b = a + 1; b < 3; ++b)
+        if (overlap(outs[a], outs[b])) return GS_ERR_ALIAS;
+    }
+    if (M == 0 || N == 0) {
+      // Empty sums: every requested gradient is zero.
+      if (M > 0) fill_zero(stream, dq, M * D);
+      if (N > 0) {
+        fill_zero(stream, dk, N * D);
+        fill_zero(stream, dv, N * C);
+      }
+      return launch_status();
+    }
+    const bool alias = (q == k) && (M == N);
+    Want w;
+    w.dq = dq != nullptr;
+    w.dk = dk != nullptr;
+    w.dv = dv != nullptr;
+    Plan pl;
+    make_plan(*p, w, alias, nullptr, pl);
+    if ((st = check_workspace(workspace, workspace_bytes, pl.total)) != GS_SUCCESS) return st;
+    Range rw = range_of(workspace, (int64_t)pl.total);
+    for (int a = 0; a < 3; ++a)
+      if (overlap(outs[a], rw)) return GS_ERR_ALIAS;
+    for (int b = 0; b < 4; ++b)
+      if (overlap(in[b], rw)) return GS_ERR_ALIAS;
+    make_plan(*p, w, alias, workspace, pl);
+
+    Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
+    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
+    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, w.dk || (alias && w.dq));
+    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, w.dq);
+    if (w.dq || w.dk) prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
+    prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
+    if (w.dq) row_bound(c, pl.q, M, pl.Mp, pl.k, N);
+    if ((w.dk || w.dv) && !alias) row_bound(c, pl.k, N, pl.Np, pl.q, M);
+    if ((w.dk || w.dv) && alias && !w.dq) row_bound(c, pl.q, M, pl.Mp, pl.k, N);
+    const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
+    if (w.dq)
+      pass_dq(c, pl.q, M, pl.k, N, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1, dq);
+    if (w.dk)
+      pass_dq(c, pl.k, N, pl.q, M, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt, pl.slots + 0, dk);
+    if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.g.ks, pl.slots + 1, dv);
+    return launch_status();
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
+
+}  // extern "C"

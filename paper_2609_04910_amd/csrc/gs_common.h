@@ -1,0 +1,111 @@
+// gs_common.h -- types, MFMA wrappers and the operand layouts shared by the
+// Gauss-sum kernels (gfx950 / CDNA4).
+//
+// Every kernel works in the transposed tile orientation S^T[n][m] = k_n . q_m
+// (keys on the MFMA row index, queries on the column index), so that the
+// 16x16 fp32 result tile of one v_mfma_f32_16x16x32 already has the register
+// layout of the B operand of the next contraction over keys.  Lane l of a
+// wave64 holds, for the 16x16x32 MFMA:
+//     A operand: A[i = l%16][k = 8*(l/16) .. +7]      (8 x 16-bit)
+//     B operand: B[k = 8*(l/16) .. +7][j = l%16]      (8 x 16-bit)
+//     result   : D[i = 4*(l/16) + r][j = l%16], r = 0..3 (4 x fp32)
+//
+// Operand storage in the workspace (all 16-byte loads, fully coalesced):
+//
+//   Row-tile layout "RT" for a matrix X (rows x W, W padded to a multiple of
+//   32): element (r, w) lives at half-index
+//       ((r/16 * (W/32) + w/32) * 16 + r%16) * 32 + w%32 ,
+//   so the 16 x 32 block needed by one MFMA operand is one contiguous 1 KiB
+//   run, and lane (i = l%16, g = l/16) reads 16 bytes at
+//       (((t * W/32 + c) * 16 + i) * 4 + g)   in 16-byte units,
+//   for row tile t and column chunk c.  Used for the contraction over D
+//   (points) and over C (values, upstream gradient).
+//
+//   Key-slot layout "KS" for a matrix Y (keys x R, R padded to 16): used as
+//   the A operand of a contraction over keys (V^T for P.V, K^T for P.K).  A
+//   32-key step s holds R rows of 32 halves; row w, slot z stores key
+//       s*32 + 16*((z%8)/4) + 4*(z/8) + z%4
+//   which is exactly the key the B operand (built from two S^T result tiles)
+//   carries in k-slot z.  Lane (i, g) reads 16 bytes at ((s*R + w0 + i)*4 + g).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gs {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlockThreads = kWave * kWavesPerBlock;
+constexpr int kStep = 32;      // keys per inner step
+constexpr int kRowPad = 256;   // row padding of every point / value array
+constexpr float kPadBias = -1.0e30f;  // -||k||^2/2 of a padding row: Phi = 0
+
+struct F16 {
+  typedef _Float16 storage;
+  static __device__ __forceinline__ float to_float(uint16_t b) {
+    return (float)__builtin_bit_cast(_Float16, b);
+  }
+};
+struct BF16 {
+  typedef __bf16 storage;
+  static __device__ __forceinline__ float to_float(uint16_t b) {
+    return __builtin_bit_cast(float, (uint32_t)b << 16);
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ floatx4 mfma_qk(uint4 a, uint4 b, floatx4 c);
+template <>
+__device__ __forceinline__ floatx4 mfma_qk<F16>(uint4 a, uint4 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a),
+                                                __builtin_bit_cast(half8, b), c, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ floatx4 mfma_qk<BF16>(uint4 a, uint4 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mfma_f16(uint4 a, uint4 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a),
+                                                __builtin_bit_cast(half8, b), c, 0, 0, 0);
+}
+
+// exp2 of the exponent, clamped to [0, 1] (folds into v_exp_f32 ... clamp):
+// the clamp is the "exponent <= 0" guarantee, so fp32 cancellation in the
+// expanded exponent can never produce a kernel value above 1.
+__device__ __forceinline__ float exp2_clamped(float x) {
+  return __builtin_amdgcn_fmed3f(__builtin_amdgcn_exp2f(x), 0.0f, 1.0f);
+}
+
+// Two fp32 -> one dword of two fp16 (round to nearest even).
+__device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
+  _Float16 a = (_Float16)lo, b = (_Float16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+// Power-of-two scale exponent e with max * 2^e in [1, 2); 0 for max = 0, Inf or NaN.
+__device__ __forceinline__ int scale_exponent(uint32_t max_bits) {
+  float mx = __builtin_bit_cast(float, max_bits);
+  if (!(mx > 0.0f) || !(mx < __builtin_inff())) return 0;
+  int e;
+  (void)frexpf(mx, &e);  // mx = f * 2^e, f in [0.5, 1)
+  return 1 - e;
+}
+
+// RT-layout half index of element (r, w) for a matrix with W (multiple of 32) columns.
+__host__ __device__ __forceinline__ int64_t rt_index(int64_t r, int w, int W) {
+  return (((r >> 4) * (W >> 5) + (w >> 5)) * 16 + (r & 15)) * 32 + (w & 31);
+}
+// KS-layout half index of element (key r, row w) for R (multiple of 16) rows.
+__host__ __device__ __forceinline__ int64_t ks_index(int64_t r, int w, int R) {
+  int o = (int)(r & 31);
+  int z = 8 * ((o & 15) >> 2) + 4 * (o >> 4) + (o & 3);
+  return ((r >> 5) * R + w) * 32 + z;
+}
+
+}  // namespace gs

@@ -1,0 +1,242 @@
+"""Thin ctypes binding of the C ABI in include/gauss_sum.h.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libgauss_sum.so``.  PyTorch provides device memory (inputs,
+outputs, workspace) and the stream.  There is no fallback: if the library is
+missing or a call fails, an exception is raised.
+
+Entry points mirror the C names:
+  gauss_sum_fwd(q, k, v, tau)                       -> s        (Eq. 1)
+  gauss_sum_bwd(q, k, v, tau, dout, want=...)       -> dq, dk, dv
+  gauss_sum_fwd_workspace_size / gauss_sum_bwd_workspace_size
+  gauss_sum_status_string / gauss_sum_abi_version
+and ``GaussSum`` wraps both in a torch.autograd.Function.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgauss_sum.so")
+
+GS_F32, GS_F16, GS_BF16 = 0, 1, 2
+STATUS = {
+    0: "GS_SUCCESS", 1: "GS_ERR_NULL_POINTER", 2: "GS_ERR_BAD_SHAPE", 3: "GS_ERR_BAD_TAU",
+    4: "GS_ERR_UNSUPPORTED", 5: "GS_ERR_MISALIGNED", 6: "GS_ERR_WORKSPACE", 7: "GS_ERR_HIP",
+    8: "GS_ERR_INTERNAL", 9: "GS_ERR_ALIAS",
+}
+EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_workspace_size",
+            "gauss_sum_bwd_workspace_size", "gauss_sum_status_string", "gauss_sum_abi_version",
+            "gauss_sum_profile_start", "gauss_sum_profile_stop")
+PROFILE_FWD, PROFILE_GRAD = 1, 2
+
+
+class GaussSumError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        msg = "%s failed: %s (%s)" % (where, STATUS.get(status, "?"), status_string(status))
+        super().__init__(msg)
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("C", ctypes.c_int64), ("qk_dtype", ctypes.c_int), ("v_dtype", ctypes.c_int)]
+
+
+_lib = None
+
+
+def load(path=LIB_PATH):
+    """Load libgauss_sum.so (built in-tree by ``__graft_entry__.build()``)."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("HIP library %s is missing: run __graft_entry__.build() first" % path)
+    lib = ctypes.CDLL(path)
+    vp, sz, f32p = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p
+    P = ctypes.POINTER(Problem)
+    lib.gauss_sum_fwd_workspace_size.argtypes = [P]
+    lib.gauss_sum_fwd_workspace_size.restype = sz
+    lib.gauss_sum_bwd_workspace_size.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    lib.gauss_sum_bwd_workspace_size.restype = sz
+    lib.gauss_sum_fwd.argtypes = [P, vp, vp, vp, ctypes.c_float, f32p, vp, sz, vp]
+    lib.gauss_sum_fwd.restype = ctypes.c_int
+    lib.gauss_sum_bwd.argtypes = [P, vp, vp, vp, ctypes.c_float, vp, ctypes.c_int, f32p, f32p, f32p,
+                                  vp, sz, vp]
+    lib.gauss_sum_bwd.restype = ctypes.c_int
+    lib.gauss_sum_status_string.argtypes = [ctypes.c_int]
+    lib.gauss_sum_status_string.restype = ctypes.c_char_p
+    lib.gauss_sum_abi_version.argtypes = []
+    lib.gauss_sum_abi_version.restype = ctypes.c_int
+    lib.gauss_sum_profile_start.argtypes = [ctypes.c_int, ctypes.c_int]
+    lib.gauss_sum_profile_start.restype = ctypes.c_int
+    lib.gauss_sum_profile_stop.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_int]
+    lib.gauss_sum_profile_stop.restype = ctypes.c_int
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def status_string(status):
+    return load().gauss_sum_status_string(int(status)).decode()
+
+
+gauss_sum_status_string = status_string
+
+
+def gauss_sum_abi_version():
+    return load().gauss_sum_abi_version()
+
+
+def gauss_sum_profile_start(capacity, kind):
+    """Start bracketing main-kernel launches of ``kind`` with HIP events."""
+    st = load().gauss_sum_profile_start(int(capacity), int(kind))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_profile_start")
+
+
+def gauss_sum_profile_stop(capacity):
+    """Per-launch durations (ms) recorded since gauss_sum_profile_start."""
+    buf = (ctypes.c_float * max(1, int(capacity)))()
+    n = load().gauss_sum_profile_stop(buf, int(capacity))
+    if n < 0:
+        raise GaussSumError(7, "gauss_sum_profile_stop")
+    return [float(buf[i]) for i in range(min(n, int(capacity)))]
+
+
+def _dtype_code(t):
+    import torch
+    codes = {torch.float32: GS_F32, torch.float16: GS_F16, torch.bfloat16: GS_BF16}
+    if t not in codes:
+        raise TypeError("unsupported dtype %s" % t)
+    return codes[t]
+
+
+def make_problem(M, N, D, C, qk_dtype, v_dtype):
+    return Problem(int(M), int(N), int(D), int(C), int(qk_dtype), int(v_dtype))
+
+
+def gauss_sum_fwd_workspace_size(M, N, D, C, qk_dtype=GS_F16, v_dtype=GS_F32):
+    return int(load().gauss_sum_fwd_workspace_size(ctypes.byref(make_problem(M, N, D, C, qk_dtype, v_dtype))))
+
+
+def gauss_sum_bwd_workspace_size(M, N, D, C, qk_dtype=GS_F16, v_dtype=GS_F32, want_dq=True,
+                                 want_dk=True, want_dv=True):
+    p = make_problem(M, N, D, C, qk_dtype, v_dtype)
+    return int(load().gauss_sum_bwd_workspace_size(ctypes.byref(p), int(bool(want_dq)),
+                                                   int(bool(want_dk)), int(bool(want_dv))))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check_inputs(q, k, v):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda:
+            raise ValueError("%s must be a GPU tensor" % name)
+        if t.dim() != 2 or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous 2-d tensor" % name)
+    if q.dtype != k.dtype:
+        raise TypeError("q and k must share a dtype")
+
+
+def _workspace(nbytes, device):
+    import torch
+    if nbytes == 0:
+        return None, 0
+    return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def gauss_sum_fwd(q, k, v, tau, out=None, workspace=None, stream=None):
+    """s = sum_n exp(-tau/2 ||q_m - k_n||^2) v_n (Eq. 1) as an M x C fp32 tensor."""
+    import torch
+    _check_inputs(q, k, v)
+    M, D = q.shape
+    N, C = v.shape
+    p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
+    lib = load()
+    if out is None:
+        out = torch.empty((M, C), dtype=torch.float32, device=q.device)
+    need = int(lib.gauss_sum_fwd_workspace_size(ctypes.byref(p)))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, q.device)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), float(tau), _ptr(out),
+                           _ptr(workspace), wbytes, _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_fwd")
+    return out
+
+
+def gauss_sum_bwd(q, k, v, tau, dout, want=(True, True, True), workspace=None, stream=None):
+    """Gradients of L = sum dout * s with respect to (q, k, v); None where not wanted."""
+    import torch
+    _check_inputs(q, k, v)
+    M, D = q.shape
+    N, C = v.shape
+    if not dout.is_cuda or dout.shape != (M, C) or not dout.is_contiguous():
+        raise ValueError("dout must be a contiguous %d x %d GPU tensor" % (M, C))
+    p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
+    lib = load()
+    dev = q.device
+    dq = torch.empty((M, D), dtype=torch.float32, device=dev) if want[0] else None
+    dk = torch.empty((N, D), dtype=torch.float32, device=dev) if want[1] else None
+    dv = torch.empty((N, C), dtype=torch.float32, device=dev) if want[2] else None
+    need = int(lib.gauss_sum_bwd_workspace_size(ctypes.byref(p), int(bool(want[0])),
+                                                int(bool(want[1])), int(bool(want[2]))))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, dev)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), float(tau), _ptr(dout),
+                           _dtype_code(dout.dtype), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace),
+                           wbytes, _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_bwd")
+    return dq, dk, dv
+
+
+def _make_autograd():
+    import torch
+
+    class GaussSum(torch.autograd.Function):
+        """s = GaussSum.apply(q, k, v, tau); gradients for q, k and v."""
+
+        @staticmethod
+        def forward(ctx, q, k, v, tau):
+            ctx.save_for_backward(q, k, v)
+            ctx.tau = float(tau)
+            return gauss_sum_fwd(q, k, v, tau)
+
+        @staticmethod
+        def backward(ctx, g):
+            q, k, v = ctx.saved_tensors
+            want = ctx.needs_input_grad[:3]
+            if not any(want):
+                return None, None, None, None
+            dq, dk, dv = gauss_sum_bwd(q, k, v, ctx.tau, g.contiguous(), want=want)
+            cast = lambda x, ref: None if x is None else x.to(ref.dtype)  # noqa: E731
+            return cast(dq, q), cast(dk, k), cast(dv, v), None
+
+    return GaussSum
+
+
+class _Lazy:
+    def __init__(self):
+        self._cls = None
+
+    def __getattr__(self, name):
+        if self._cls is None:
+            self._cls = _make_autograd()
+        return getattr(self._cls, name)
+
+
+GaussSum = _Lazy()

@@ -1,0 +1,129 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and rejects bad arguments before enqueuing any GPU work (these
+calls use fake device addresses; validation never dereferences them)."""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_04910_amd import gauss_sum as gs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gauss_sum.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gauss_sum_\w+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = gs.load()
+    names = declared_functions()
+    assert set(names) == set(gs.EXPORTED), names
+    out = subprocess.run(["nm", "-D", "--defined-only", gs.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (\w+)", out))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(lib, n)
+
+
+def test_abi_version_and_status_strings():
+    assert gs.gauss_sum_abi_version() == 1
+    seen = set()
+    for code in range(10):
+        s = gs.status_string(code)
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 10
+    assert gs.status_string(1234) == "unknown status"
+
+
+FAKE = 0x100000  # a 256-aligned fake device address, never dereferenced
+
+
+def _fwd(M=8, N=8, D=4, C=2, qk=gs.GS_F16, vd=gs.GS_F32, q=FAKE, k=FAKE + 0x10000,
+         v=FAKE + 0x20000, tau=1.0, out=FAKE + 0x30000, ws=FAKE + 0x100000, wsb=1 << 40, p=True):
+    lib = gs.load()
+    prob = gs.make_problem(M, N, D, C, qk, vd)
+    pp = ctypes.byref(prob) if p else None
+    return lib.gauss_sum_fwd(pp, q, k, v, ctypes.c_float(tau), out, ws, wsb, None)
+
+
+def _bwd(M=8, N=8, D=4, C=2, qk=gs.GS_F16, vd=gs.GS_F32, gd=gs.GS_F32, tau=1.0,
+         dq=FAKE + 0x40000, dk=FAKE + 0x50000, dv=FAKE + 0x60000, dout=FAKE + 0x70000,
+         ws=FAKE + 0x100000, wsb=1 << 40):
+    lib = gs.load()
+    prob = gs.make_problem(M, N, D, C, qk, vd)
+    return lib.gauss_sum_bwd(ctypes.byref(prob), FAKE, FAKE + 0x10000, FAKE + 0x20000,
+                             ctypes.c_float(tau), dout, gd, dq, dk, dv, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(p=False), 1),
+    (dict(q=None), 1), (dict(k=None), 1), (dict(v=None), 1), (dict(out=None), 1),
+    (dict(M=-1), 2), (dict(N=-3), 2), (dict(D=0), 2), (dict(D=257), 2), (dict(C=0), 2),
+    (dict(C=300), 2), (dict(M=1 << 40), 2),
+    (dict(tau=0.0), 3), (dict(tau=-1.0), 3), (dict(tau=float("nan")), 3),
+    (dict(tau=float("inf")), 3),
+    (dict(qk=gs.GS_F32), 4), (dict(qk=7), 4), (dict(vd=9), 4),
+    (dict(q=FAKE + 1), 5), (dict(v=FAKE + 0x20002), 5), (dict(out=FAKE + 0x30002), 5),
+    (dict(ws=FAKE + 0x100010), 5),
+    (dict(ws=None), 6), (dict(wsb=16), 6),
+    (dict(out=FAKE + 0x10000), 9), (dict(out=FAKE + 0x20004), 9), (dict(ws=FAKE + 0x30000 - 256), 9),
+])
+def test_fwd_validation(kw, status):
+    assert _fwd(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dq=None, dk=None, dv=None), 1), (dict(dout=None), 1),
+    (dict(gd=5), 4), (dict(D=300), 2), (dict(tau=-2.0), 3),
+    (dict(dq=FAKE + 0x40002), 5), (dict(dout=FAKE + 0x70002), 5),
+    (dict(dq=FAKE + 0x10000), 9), (dict(dk=FAKE + 0x40000), 9), (dict(dv=FAKE + 0x70000), 9),
+    (dict(wsb=1), 6), (dict(ws=None), 6),
+])
+def test_bwd_validation(kw, status):
+    assert _bwd(**kw) == status
+
+
+def test_empty_query_set_is_a_noop():
+    # M = 0: nothing to compute; no pointer is touched and no kernel runs.
+    assert _fwd(M=0, q=None, out=None) == 0
+
+
+def test_workspace_sizes():
+    assert gs.gauss_sum_fwd_workspace_size(0, 5, 3, 1) == 0
+    assert gs.gauss_sum_fwd_workspace_size(5, 0, 3, 1) == 0
+    assert gs.gauss_sum_fwd_workspace_size(5, 5, 0, 1) == 0  # invalid
+    a = gs.gauss_sum_fwd_workspace_size(4096, 4096, 16, 1)
+    b = gs.gauss_sum_fwd_workspace_size(8192, 8192, 16, 1)
+    assert 0 < a < b and a % 256 == 0
+    assert gs.gauss_sum_bwd_workspace_size(64, 64, 8, 2, want_dq=False, want_dk=False,
+                                           want_dv=False) == 0
+    full = gs.gauss_sum_bwd_workspace_size(1000, 3000, 64, 4)
+    only_dq = gs.gauss_sum_bwd_workspace_size(1000, 3000, 64, 4, want_dk=False, want_dv=False)
+    assert 0 < only_dq < full
+
+
+def test_profile_hook_arguments():
+    lib = gs.load()
+    assert lib.gauss_sum_profile_start(0, 1) == 2
+    assert lib.gauss_sum_profile_start(4, 0) == 2
+    assert lib.gauss_sum_profile_start(4, 4) == 2
+    assert lib.gauss_sum_profile_stop(None, 0) == 0  # nothing started
+
+
+def test_no_device_reports_hip_error():
+    # A valid call in a process without a usable GPU fails at launch, and the
+    # failure is reported as GS_ERR_HIP rather than crashing.
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is visible")
+    assert _fwd() == 7
+    assert _bwd() == 7

@@ -1,0 +1,190 @@
+"""GPU parity: the HIP library (called through the C ABI) against the fp64
+oracle, element by element, on seeded inputs.
+
+Small shapes are compared on every output element; the five benchmark
+workloads run at full size in the launch configuration the benchmark times,
+compared on sampled rows (each sampled row against all partners, so every
+checked element is exact, not an estimate).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2609_04910_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    from paper_2609_04910_amd import gauss_sum as gs
+    gs.load()
+    yield
+
+
+# (M, N, D, C, qk dtype, v dtype, dout dtype, tau or None (= 1/D), spread)
+SHAPES = [
+    (1, 1, 1, 1, "f16", "f32", "f32", 0.7, 1.0),
+    (7, 5, 3, 2, "f16", "f32", "f32", None, 1.0),
+    (63, 65, 16, 1, "f16", "f32", "f32", None, 1.0),
+    (64, 64, 32, 4, "bf16", "f32", "f32", None, 1.0),
+    (65, 129, 17, 15, "f16", "f16", "f16", None, 1.0),
+    (127, 63, 33, 16, "f16", "f32", "f32", 0.2, 1.0),
+    (129, 300, 64, 17, "bf16", "f16", "f32", None, 1.0),
+    (200, 333, 100, 32, "f16", "f32", "f16", None, 1.0),
+    (300, 257, 128, 128, "f16", "f16", "f32", None, 1.0),
+    (100, 150, 255, 3, "f16", "f32", "f32", None, 1.0),
+    (96, 200, 256, 256, "f16", "f32", "f32", None, 1.0),
+    (257, 97, 8, 64, "bf16", "f32", "f32", 0.5, 1.0),
+    (33, 1000, 15, 1, "f16", "f32", "f32", None, 1.0),
+    (1000, 33, 1, 8, "f16", "f32", "f32", 2.0, 1.0),
+    # kernel values far below 2^-8 for every query: exercises the exact
+    # row-maximum shift
+    (150, 400, 8, 4, "f16", "f32", "f32", 3.0, 3.0),
+    (150, 400, 32, 2, "bf16", "f32", "f32", 10.0, 2.0),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "M%d_N%d_D%d_C%d_%s_v%s_g%s" % s[:7])
+def test_small_shapes_all_outputs(shape):
+    import parity
+    M, N, D, C, qk, vd, gd, tau, spread = shape
+    _say("case", shape)
+    w = parity.random_workload(SHAPES.index(shape), M, N, D, C, qk, vd, gd, tau, spread)
+    stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
+    _say("  max err/A and rel-L2:", stats)
+
+
+def test_same_points_alias_matches_separate_arrays():
+    import parity
+    w = parity.random_workload(5, 300, 300, 24, 3, same=True)
+    a = parity.run(w, ("fwd", "dq", "dk", "dv"), alias=True)
+    b = parity.run(w, ("fwd", "dq", "dk", "dv"), alias=False)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+    parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
+
+
+def test_deterministic_bitwise():
+    import parity
+    w = parity.random_workload(6, 2000, 3000, 48, 8)
+    a = parity.run(w, ("fwd", "dq", "dk", "dv"))
+    b = parity.run(w, ("fwd", "dq", "dk", "dv"))
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_power_of_two_linearity_bitwise():
+    import parity
+    w = parity.random_workload(7, 500, 700, 20, 5)
+    a = parity.run(w, ("fwd",))["fwd"]
+    w.v = (w.v * np.float32(8.0)).astype(w.v.dtype)
+    b = parity.run(w, ("fwd",))["fwd"]
+    assert np.array_equal(b, a * np.float32(8.0))
+
+
+def test_empty_and_degenerate():
+    import torch
+    from paper_2609_04910_amd import gauss_sum as gs
+    dev = "cuda"
+    q = torch.randn(37, 5, device=dev).half()
+    k0 = torch.empty(0, 5, device=dev).half()
+    v0 = torch.empty(0, 3, device=dev)
+    out = gs.gauss_sum_fwd(q, k0, v0, 1.0)
+    torch.cuda.synchronize()
+    assert out.shape == (37, 3) and torch.all(out == 0)
+    dq, dk, dv = gs.gauss_sum_bwd(q, k0, v0, 1.0, torch.randn(37, 3, device=dev))
+    torch.cuda.synchronize()
+    assert torch.all(dq == 0) and dk.shape == (0, 5) and dv.shape == (0, 3)
+    q0 = torch.empty(0, 5, device=dev).half()
+    k = torch.randn(11, 5, device=dev).half()
+    v = torch.randn(11, 3, device=dev)
+    out = gs.gauss_sum_fwd(q0, k, v, 1.0)
+    dq, dk, dv = gs.gauss_sum_bwd(q0, k, v, 1.0, torch.empty(0, 3, device=dev))
+    torch.cuda.synchronize()
+    assert out.shape == (0, 3) and torch.all(dk == 0) and torch.all(dv == 0)
+    # a point against itself: s = v within the fp16 rounding of v
+    x = torch.randn(1, 7, device=dev).half()
+    v1 = torch.tensor([[0.3, -2.5]], device=dev)
+    s = gs.gauss_sum_fwd(x, x, v1, 5.0)
+    torch.cuda.synchronize()
+    assert torch.allclose(s, v1, rtol=2 ** -11, atol=0)
+
+
+def test_zero_value_rows_give_exactly_zero_key_gradient():
+    import parity
+    w = parity.random_workload(8, 400, 600, 40, 6)
+    zero = np.arange(0, 600, 7)
+    w.v[zero] = 0
+    got = parity.run(w, ("dk",))["dk"]
+    assert np.all(got[zero] == 0)
+    parity.check_workload(w, passes=("dk", "dv"))
+
+
+# ------------------------------------------------ benchmark workloads
+
+REDUCED = {
+    "dense_d16": dict(M=4096, N=4096),
+    "mmd_flow": dict(M=3000, N=3000),
+    "svgd": dict(M=1500, N=1500),
+    "mixture_d32": dict(M=5000, N=5000),
+    "rect_d256": dict(M=700, N=3000),
+}
+
+
+@pytest.mark.parametrize("name", wl.ORDER)
+def test_workload_reduced_size_all_rows(name):
+    import parity
+    taus = wl.MIXTURE_TAUS if name == "mixture_d32" else (None,)
+    for tau in taus:
+        w = wl.make(name, seed=0, tau=tau, **REDUCED[name])
+        _say("workload", name, "tau", w.tau, "M", w.M, "N", w.N)
+        stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
+        _say("  stats", stats)
+
+
+# Sampled query rows / key rows per workload, sized so the oracle checks each
+# in seconds (None = every row).
+SAMPLES = {
+    "dense_d16": (None, None),
+    "mmd_flow": (1024, 1024),
+    "svgd": (1024, 1024),
+    "mixture_d32": (1024, 1024),
+    "rect_d256": (96, 1024),
+}
+
+
+@pytest.mark.parametrize("name", wl.ORDER)
+def test_workload_full_size_sampled_rows(name):
+    import parity
+    taus = wl.MIXTURE_TAUS if name == "mixture_d32" else (None,)
+    nq, nk = SAMPLES[name]
+    for tau in taus:
+        w = wl.make(name, seed=0, tau=tau)
+        rows = None if nq is None else wl.sample_rows(w.M, nq, seed=1)
+        key_rows = None if nk is None else wl.sample_rows(w.N, nk, seed=2)
+        _say("workload", name, "tau", w.tau, "full size", w.M, w.N)
+        stats = parity.check_workload(w, rows=rows, key_rows=key_rows)
+        _say("  stats", stats)
+
+
+def test_mixture_tau10_adversarial_rows():
+    """The 64 queries with the smallest sum of kernel values (found on the GPU
+    with v = 1) are the hardest for fp16 kernel values; check them exactly."""
+    import parity
+    w = wl.make("mixture_d32", seed=0, tau=10.0)
+    ones = wl.Workload(w.name, w.M, w.N, w.D, 1, w.tau, w.qk_dtype, w.q, w.k,
+                       np.ones((w.N, 1), np.float32), None, ("fwd",), False, w.q_values, w.k_values)
+    sums = parity.run(ones, ("fwd",))["fwd"][:, 0]
+    rows = np.sort(np.argsort(sums)[:64])
+    _say("smallest row sums", sums[rows[:4]])
+    parity.check_workload(w, passes=("fwd",), rows=rows)
