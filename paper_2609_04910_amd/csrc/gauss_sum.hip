@@ -19,7 +19,6 @@ namespace gs {
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kRowBoundSamples = 64;
 constexpr int kTargetBlocks = 1024;   // workgroups per pass before splitting over keys
 constexpr int kMinStepsPerSplit = 4;  // 128 keys
 
@@ -51,42 +50,38 @@ inline Dims dims_of(int64_t D, int64_t C) {
 }
 
 // Query tiles per wave: the largest of 4, 2, 1 whose kernel (as compiled for
-// gfx950) needs at most 256 registers per lane, i.e. keeps two waves per SIMD;
-// the D = 256 gradient kernel needs ~280 at one tile and runs one wave per SIMD.
+// gfx950) keeps the register count at or below 256 per lane (two waves per
+// SIMD); the D = 256 gradient kernel runs one wave per SIMD.
 constexpr int fwd_qt(int DP, int CT) {
   return CT >= 16 ? 1 : CT == 8 ? 2 : (DP == 8 && CT > 1) ? 2 : 4;
 }
 constexpr int dq_qt(int DP, int CW) {
-  return DP >= 4 ? 1 : DP == 2 ? 2 : CW >= 4 ? 2 : 4;
+  return DP >= 4 ? 1 : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
 }
 
 // ------------------------------------------------------------ dispatch tables
 
-template <typename T, int DP, int CT, int QT>
-void launch_fwd_q(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const float* Lq,
-                  const uint4* ks, const float* nhk, const uint4* vt, const uint32_t* vslot,
-                  float tau2, int64_t M, int C, int steps, int sps, float* out, int64_t pstride) {
-  hipLaunchKernelGGL((k_fwd<T, DP, CT, QT>), grid, dim3(kBlockThreads), 0, st, qs, nhq, Lq, ks, nhk,
-                     vt, vslot, tau2, M, C, steps, sps, out, pstride);
-}
-
-using FwdFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const float*, const uint4*,
-                       const float*, const uint4*, const uint32_t*, float, int64_t, int, int, int,
-                       float*, int64_t);
+using FwdFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
+                       const uint4*, const float*, const uint4*, const uint32_t*, float, int64_t, int,
+                       int, int, float*, int64_t);
 
 template <typename T, int DP, int CT>
-constexpr FwdFn fwd_entry() {
-  return &launch_fwd_q<T, DP, CT, fwd_qt(DP, CT)>;
+void launch_fwd(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const uint4* srt,
+                const float* snh, const uint4* ks, const float* scal, const uint4* vt,
+                const uint32_t* vslot, float tau2, int64_t M, int C, int steps, int sps, float* out,
+                int64_t pstride) {
+  hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT)>), grid, dim3(kBlockThreads), 0, st, qs, nhq,
+                     srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride);
 }
 
 template <typename T, int DP>
 FwdFn fwd_by_ct(int CT) {
   switch (CT) {
-    case 1: return fwd_entry<T, DP, 1>();
-    case 2: return fwd_entry<T, DP, 2>();
-    case 4: return fwd_entry<T, DP, 4>();
-    case 8: return fwd_entry<T, DP, 8>();
-    case 16: return fwd_entry<T, DP, 16>();
+    case 1: return &launch_fwd<T, DP, 1>;
+    case 2: return &launch_fwd<T, DP, 2>;
+    case 4: return &launch_fwd<T, DP, 4>;
+    case 8: return &launch_fwd<T, DP, 8>;
+    case 16: return &launch_fwd<T, DP, 16>;
   }
   return nullptr;
 }
@@ -102,33 +97,30 @@ FwdFn fwd_fn(int DP, int CT) {
   return nullptr;
 }
 
-template <typename T, int DP, int CW, int QT>
-void launch_dq_q(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const float* Lq,
-                 const uint4* ks, const float* nhk, const uint4* kt, const uint32_t* kslot,
-                 const uint4* vs, const uint32_t* vslot, const uint4* gsr, const uint32_t* gslot,
-                 float tau2, float tau, int64_t M, int D, int steps, int sps, float* out,
-                 int64_t pstride) {
-  hipLaunchKernelGGL((k_dq<T, DP, CW, QT>), grid, dim3(kBlockThreads), 0, st, qs, nhq, Lq, ks, nhk,
-                     kt, kslot, vs, vslot, gsr, gslot, tau2, tau, M, D, steps, sps, out, pstride);
-}
-
-using DqFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const float*, const uint4*,
-                      const float*, const uint4*, const uint32_t*, const uint4*, const uint32_t*,
-                      const uint4*, const uint32_t*, float, float, int64_t, int, int, int, float*,
-                      int64_t);
+using DqFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
+                      const uint4*, const float*, const uint4*, const uint32_t*, const uint4*,
+                      const uint32_t*, const uint4*, const uint32_t*, float, float, int64_t, int, int,
+                      int, float*, int64_t);
 
 template <typename T, int DP, int CW>
-constexpr DqFn dq_entry() {
-  return &launch_dq_q<T, DP, CW, dq_qt(DP, CW)>;
+void launch_dq(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const uint4* srt,
+               const float* snh, const uint4* ks, const float* scal, const uint4* kt,
+               const uint32_t* kslot, const uint4* vs, const uint32_t* vslot, const uint4* gsr,
+               const uint32_t* gslot, float tau2, float tau, int64_t M, int D, int steps, int sps,
+               float* out, int64_t pstride) {
+  hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW)>), grid, dim3(kBlockThreads), 0, st, qs, nhq,
+                     srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, tau2, tau, M, D, steps, sps,
+                     out, pstride);
 }
 
 template <typename T, int DP>
 DqFn dq_by_cw(int CW) {
   switch (CW) {
-    case 1: return dq_entry<T, DP, 1>();
-    case 2: return dq_entry<T, DP, 2>();
-    case 4: return dq_entry<T, DP, 4>();
-    case 8: return dq_entry<T, DP, 8>();
+    case 0: return &launch_dq<T, DP, 0>;
+    case 1: return &launch_dq<T, DP, 1>;
+    case 2: return &launch_dq<T, DP, 2>;
+    case 4: return &launch_dq<T, DP, 4>;
+    case 8: return &launch_dq<T, DP, 8>;
   }
   return nullptr;
 }
@@ -158,10 +150,11 @@ struct Carver {
 };
 
 struct Side {  // one point set with the arrays derived from it
-  uint16_t* rt = nullptr;  // RT copy (input dtype)
-  float* nh = nullptr;     // -||x||^2/2
-  float* L = nullptr;      // sampled row bound (as queries against the other set)
-  uint16_t* ks = nullptr;  // KS fp16 copy (operand of sum_n P k_n)
+  uint16_t* rt = nullptr;       // RT copy (input dtype)
+  float* nh = nullptr;          // -||x||^2/2 (padding rows: kPadBias)
+  uint16_t* ks = nullptr;       // KS fp16 copy (operand of sum_n P k_n)
+  uint16_t* samp_rt = nullptr;  // 64 sampled rows, RT layout
+  float* samp_nh = nullptr;     // their half norms
 };
 
 struct Vals {  // one value set (v or dout)
@@ -172,22 +165,23 @@ struct Vals {  // one value set (v or dout)
 struct Plan {
   Dims dm;
   int64_t Mp = 0, Np = 0;
-  bool alias = false;  // q and k are the same array
-  uint32_t* slots = nullptr;  // [0] |v| max, [1] |dout| max, [2] |q| max, [3] |k| max
+  bool alias = false;          // q and k are the same array
+  uint32_t* slots = nullptr;   // [0] |v| max, [1] |dout| max, [2] |q| max, [3] |k| max
   Side q, k;
   Vals v, g;
+  float* scal_kv = nullptr;    // per-step scalars, keys k with values v
+  float* scal_qg = nullptr;    // per-step scalars, keys q with values dout
   float* part = nullptr;
   size_t part_bytes = 0;
   size_t total = 0;
 };
 
 struct PassShape {
-  int QT, blocks, splits, sps, steps;
+  int blocks, splits, sps, steps;
 };
 
 PassShape pass_shape(int64_t rows, int64_t keys, int QT) {
   PassShape ps;
-  ps.QT = QT;
   ps.blocks = (int)ceil_div(rows, 64 * QT);
   ps.steps = (int)ceil_div(keys, kStep);
   int want = (int)std::max<int64_t>(1, ceil_div(kTargetBlocks, std::max(1, ps.blocks)));
@@ -202,6 +196,8 @@ struct Want {
   bool fwd = false, dq = false, dk = false, dv = false;
 };
 
+inline int dq_cw(const gs_problem& p, const Dims& dm) { return p.C == 1 ? 0 : dm.CW; }
+
 // Lays out every buffer the requested passes need; with ws == nullptr only
 // computes the size.
 void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& pl) {
@@ -213,20 +209,27 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   Carver cv;
   cv.base = static_cast<char*>(ws);
   pl.slots = cv.take<uint32_t>(64);
+  const bool keys_k = w.fwd || w.dq;  // passes whose keys are k
+  const bool keys_q = w.dk || w.dv;   // passes whose keys are q
   const bool need_k_ks = w.dq, need_q_ks = w.dk;
-  const bool need_Lk = w.dk || w.dv;
-  pl.q.rt = cv.take<uint16_t>(pl.Mp * W * 2);
-  pl.q.nh = cv.take<float>(pl.Mp * 4);
-  pl.q.L = cv.take<float>(pl.Mp * 4);
-  if (need_q_ks || (alias && need_k_ks)) pl.q.ks = cv.take<uint16_t>(pl.Mp * W * 2);
+  auto side = [&](Side& s, int64_t n_pad, bool ks, bool sample) {
+    s.rt = cv.take<uint16_t>(n_pad * W * 2);
+    s.nh = cv.take<float>(n_pad * 4);
+    if (ks) s.ks = cv.take<uint16_t>(n_pad * W * 2);
+    if (sample) {
+      s.samp_rt = cv.take<uint16_t>(64 * W * 2);
+      s.samp_nh = cv.take<float>(64 * 4);
+    }
+  };
   if (alias) {
+    side(pl.q, pl.Mp, need_q_ks || need_k_ks, true);
     pl.k = pl.q;
   } else {
-    pl.k.rt = cv.take<uint16_t>(pl.Np * W * 2);
-    pl.k.nh = cv.take<float>(pl.Np * 4);
-    if (need_Lk) pl.k.L = cv.take<float>(pl.Np * 4);
-    if (need_k_ks) pl.k.ks = cv.take<uint16_t>(pl.Np * W * 2);
+    side(pl.q, pl.Mp, need_q_ks, keys_q);
+    side(pl.k, pl.Np, need_k_ks, keys_k);
   }
+  if (keys_k) pl.scal_kv = cv.take<float>(pl.Np * 2 * 4);
+  if (keys_q) pl.scal_qg = cv.take<float>(pl.Mp * 2 * 4);
   if (w.dq || w.dk) pl.v.rt = cv.take<uint16_t>(pl.Np * Wv * 2);
   if (w.fwd) pl.v.ks = cv.take<uint16_t>(pl.Np * Rv * 2);
   if (w.dq || w.dk) pl.g.rt = cv.take<uint16_t>(pl.Mp * Wv * 2);
@@ -238,7 +241,7 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
     PassShape ps = pass_shape(rows, keys, QT);
     if (ps.splits > 1) part = std::max(part, (size_t)ps.splits * rows * width * 4);
   };
-  const int qf = fwd_qt(pl.dm.DP, pl.dm.CT), qd = dq_qt(pl.dm.DP, pl.dm.CW);
+  const int qf = fwd_qt(pl.dm.DP, pl.dm.CT), qd = dq_qt(pl.dm.DP, dq_cw(p, pl.dm));
   if (w.fwd) consider(p.M, p.N, qf, p.C);
   if (w.dq) consider(p.M, p.N, qd, p.D);
   if (w.dk) consider(p.N, p.M, qd, p.D);
@@ -290,30 +293,36 @@ struct Ctx {
   float tau, tau2;
 };
 
-void prep_points(const Ctx& c, const void* x, int64_t n, int64_t n_pad, Side& s, uint32_t* slot,
-                 bool ks_copy) {
+template <typename T>
+void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t n, int64_t n_pad, Side& s,
+                   uint32_t* slot) {
   const gs_problem& p = *c.p;
   const int W = c.pl->dm.W();
-  const uint16_t* x16 = static_cast<const uint16_t*>(x);
   hipLaunchKernelGGL(k_points_rt, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D, n_pad,
                      W, s.rt);
-  if (p.qk_dtype == GS_F16)
-    hipLaunchKernelGGL(k_points_norm<F16>, dim3(grid1(n_pad)), dim3(256), 0, c.st, x16, n, (int)p.D,
-                       n_pad, s.nh);
-  else
-    hipLaunchKernelGGL(k_points_norm<BF16>, dim3(grid1(n_pad)), dim3(256), 0, c.st, x16, n, (int)p.D,
-                       n_pad, s.nh);
-  if (ks_copy) {
-    if (p.qk_dtype == GS_F16) {
-      hipLaunchKernelGGL(k_points_ks<F16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n,
-                         (int)p.D, n_pad, W, (const uint32_t*)nullptr, s.ks);
-    } else {
-      hipLaunchKernelGGL(k_absmax, dim3(grid1(n * p.D, 256)), dim3(256), 0, c.st, x, n * p.D, 2,
-                         slot);
-      hipLaunchKernelGGL(k_points_ks<BF16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n,
-                         (int)p.D, n_pad, W, (const uint32_t*)slot, s.ks);
+  hipLaunchKernelGGL(k_points_norm<T>, dim3(grid1(n_pad)), dim3(256), 0, c.st, x16, n, (int)p.D, n_pad,
+                     s.nh);
+  if (s.samp_rt)
+    hipLaunchKernelGGL(k_sample<T>, dim3(grid1(64 * W)), dim3(256), 0, c.st, x16, n, (int)p.D, W,
+                       s.samp_rt, s.samp_nh);
+  if (s.ks) {
+    const uint32_t* sl = nullptr;
+    if (p.qk_dtype == GS_BF16) {
+      hipLaunchKernelGGL(k_absmax, dim3(grid1(n * p.D, 256)), dim3(256), 0, c.st,
+                         static_cast<const void*>(x16), n * p.D, 2, slot);
+      sl = slot;
     }
+    hipLaunchKernelGGL(k_points_ks<T>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
+                       n_pad, W, sl, s.ks);
   }
+}
+
+void prep_points(const Ctx& c, const void* x, int64_t n, int64_t n_pad, Side& s, uint32_t* slot) {
+  const uint16_t* x16 = static_cast<const uint16_t*>(x);
+  if (c.p->qk_dtype == GS_F16)
+    prep_points_t<F16>(c, x16, n, n_pad, s, slot);
+  else
+    prep_points_t<BF16>(c, x16, n, n_pad, s, slot);
 }
 
 void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t n, int64_t n_pad, Vals& s,
@@ -331,18 +340,13 @@ void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t n, int64_t n_
                        (int)p.C, n_pad, Rv, (const uint32_t*)slot, s.ks);
 }
 
-void row_bound(const Ctx& c, const Side& qside, int64_t nq, int64_t nq_pad, const Side& kside,
-               int64_t nk) {
-  const gs_problem& p = *c.p;
-  const int W = c.pl->dm.W();
-  const int samples = (int)std::min<int64_t>(kRowBoundSamples, std::max<int64_t>(nk, 1));
-  if (p.qk_dtype == GS_F16)
-    hipLaunchKernelGGL(k_row_bound<F16>, dim3(grid1(nq_pad)), dim3(256), 0, c.st, qside.rt, qside.nh,
-                       nq, nq_pad, kside.rt, kside.nh, nk, (int)p.D, W, c.tau2, samples, qside.L);
-  else
-    hipLaunchKernelGGL(k_row_bound<BF16>, dim3(grid1(nq_pad)), dim3(256), 0, c.st, qside.rt,
-                       qside.nh, nq, nq_pad, kside.rt, kside.nh, nk, (int)p.D, W, c.tau2, samples,
-                       qside.L);
+// Per-step key scalars of key side `s` paired with values x (slot = their
+// absolute maximum), for C = 1 gradient passes; half norms only otherwise.
+void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64_t n, int64_t n_pad,
+                  const uint32_t* slot, float* out) {
+  const bool vals = c.p->C == 1 && x != nullptr;
+  hipLaunchKernelGGL(k_step_scalars, dim3(grid1(n_pad * 2)), dim3(256), 0, c.st, (const float*)s.nh,
+                     vals ? x : nullptr, (int)dt, n, (int)c.p->C, n_pad, vals ? slot : nullptr, out);
 }
 
 void combine(const Ctx& c, const PassShape& ps, int64_t count, float* out) {
@@ -353,34 +357,35 @@ void combine(const Ctx& c, const PassShape& ps, int64_t count, float* out) {
 
 // Forward-type pass: out[m, :] = sum_n Phi(x_m, y_n) val_n for x = qside rows.
 void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk,
-              const uint16_t* vks, const uint32_t* vslot, float* out) {
+              const float* scal, const uint16_t* vks, const uint32_t* vslot, float* out) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
   PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT));
   FwdFn fn = p.qk_dtype == GS_F16 ? fwd_fn<F16>(dm.DP, dm.CT) : fwd_fn<BF16>(dm.DP, dm.CT);
   float* dst = ps.splits > 1 ? c.pl->part : out;
   prof_before(kKindFwd, c.st);
-  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, qs.L, (const uint4*)ks.rt, ks.nh,
-     (const uint4*)vks, vslot, c.tau2, nq, (int)p.C, ps.steps, ps.sps, dst,
-     ps.splits > 1 ? nq * p.C : 0);
+  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
+     ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)vks, vslot, c.tau2, nq, (int)p.C, ps.steps,
+     ps.sps, dst, ps.splits > 1 ? nq * p.C : 0);
   prof_after(kKindFwd, c.st);
   combine(c, ps, nq * p.C, out);
 }
 
 // dq-type pass: out[m, :] = tau sum_n Phi(x_m, y_n) <gx_m, vy_n> (y_n - x_m).
-void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const uint32_t* kslot,
-             const uint16_t* vrt, const uint32_t* vslot, const uint16_t* grt, const uint32_t* gslot,
-             float* out) {
+void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const float* scal,
+             const uint32_t* kslot, const uint16_t* vrt, const uint32_t* vslot, const uint16_t* grt,
+             const uint32_t* gslot, float* out) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
-  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, dm.CW));
-  DqFn fn = p.qk_dtype == GS_F16 ? dq_fn<F16>(dm.DP, dm.CW) : dq_fn<BF16>(dm.DP, dm.CW);
+  const int cw = dq_cw(p, dm);
+  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, cw));
+  DqFn fn = p.qk_dtype == GS_F16 ? dq_fn<F16>(dm.DP, cw) : dq_fn<BF16>(dm.DP, cw);
   float* dst = ps.splits > 1 ? c.pl->part : out;
   prof_before(kKindGrad, c.st);
-  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, qs.L, (const uint4*)ks.rt, ks.nh,
-     (const uint4*)ks.ks, p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot,
-     (const uint4*)grt, gslot, c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst,
-     ps.splits > 1 ? nq * p.D : 0);
+  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
+     ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)ks.ks,
+     p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot, (const uint4*)grt, gslot,
+     c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst, ps.splits > 1 ? nq * p.D : 0);
   prof_after(kKindGrad, c.st);
   combine(c, ps, nq * p.D, out);
 }
@@ -550,11 +555,11 @@ gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const
 
     Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
     hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
-    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, false);
-    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, false);
+    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2);
+    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3);
     prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
-    row_bound(c, pl.q, M, pl.Mp, pl.k, N);
-    pass_fwd(c, pl.q, M, pl.k, N, pl.v.ks, pl.slots + 0, out);
+    prep_scalars(c, pl.k, nullptr, p->v_dtype, N, pl.Np, nullptr, pl.scal_kv);
+    pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out);
     return launch_status();
   } catch (...) {
     return GS_ERR_INTERNAL;
@@ -613,19 +618,20 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
 
     Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
     hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
-    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, w.dk || (alias && w.dq));
-    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, w.dq);
+    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2);
+    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3);
     if (w.dq || w.dk) prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
     prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
-    if (w.dq) row_bound(c, pl.q, M, pl.Mp, pl.k, N);
-    if ((w.dk || w.dv) && !alias) row_bound(c, pl.k, N, pl.Np, pl.q, M);
-    if ((w.dk || w.dv) && alias && !w.dq) row_bound(c, pl.q, M, pl.Mp, pl.k, N);
+    if (pl.scal_kv) prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
+    if (pl.scal_qg) prep_scalars(c, pl.q, dout, dout_dtype, M, pl.Mp, pl.slots + 1, pl.scal_qg);
     const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
     if (w.dq)
-      pass_dq(c, pl.q, M, pl.k, N, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1, dq);
+      pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1,
+              dq);
     if (w.dk)
-      pass_dq(c, pl.k, N, pl.q, M, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt, pl.slots + 0, dk);
-    if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.g.ks, pl.slots + 1, dv);
+      pass_dq(c, pl.k, N, pl.q, M, pl.scal_qg, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt,
+              pl.slots + 0, dk);
+    if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv);
     return launch_status();
   } catch (...) {
     return GS_ERR_INTERNAL;

@@ -82,10 +82,12 @@ __device__ __forceinline__ float exp2_clamped(float x) {
   return __builtin_amdgcn_fmed3f(__builtin_amdgcn_exp2f(x), 0.0f, 1.0f);
 }
 
-// Two fp32 -> one dword of two fp16 (round to nearest even).
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef _Float16 halfx2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> one dword of two fp16, round to nearest even (one v_cvt_pk_f16_f32).
 __device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
-  _Float16 a = (_Float16)lo, b = (_Float16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, halfx2));
 }
 
 // Power-of-two scale exponent e with max * 2^e in [1, 2); 0 for max = 0, Inf or NaN.

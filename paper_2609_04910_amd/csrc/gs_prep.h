@@ -130,27 +130,46 @@ __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, in
   }
 }
 
-// Row bound: L[m] = max over a strided sample of keys of the log2 kernel value
-// tau' * (q_m.k_n - ||q_m||^2/2 - ||k_n||^2/2), from the RT copies.  Rows past
-// M get 0 (they never force the shifted evaluation).
+// Row-bound sample: rows n_j = floor(j N / 64), j < 64, of a point set, in
+// RT layout (64 rows, W columns, input dtype) with their half norms; with
+// N < 64 the rows j < N and padding (zero point, kPadBias norm) after.
 template <typename T>
-__global__ void k_row_bound(const uint16_t* __restrict__ qs, const float* __restrict__ nhq, int64_t M,
-                            int64_t m_pad, const uint16_t* __restrict__ ks,
-                            const float* __restrict__ nhk, int64_t N, int D, int W, float tau2,
-                            int samples, float* __restrict__ L) {
+__global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W,
+                         uint16_t* __restrict__ srt, float* __restrict__ snh) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= 64 * W) return;
+  const int j = t / W, w = t - (t / W) * W;
+  const bool real = n >= 64 || j < n;
+  const int64_t r = n >= 64 ? ((int64_t)j * n) / 64 : j;
+  srt[rt_index(j, w, W)] = (real && w < D) ? x[r * D + w] : (uint16_t)0;
+  if (w == 0) {
+    double acc = 0.0;
+    if (real)
+      for (int d = 0; d < D; ++d) {
+        double v = (double)T::to_float(x[r * D + d]);
+        acc += v * v;
+      }
+    snh[j] = real ? (float)(-0.5 * acc) : kPadBias;
+  }
+}
+
+// Per-step key scalars: for step s, 32 half norms followed by 32 scaled
+// single-channel values (v * 2^e, e from *slot; zeros when C > 1 or no values).
+__global__ void k_step_scalars(const float* __restrict__ nh, const void* __restrict__ v, int dtype,
+                               int64_t n, int C, int64_t n_pad, const uint32_t* __restrict__ slot,
+                               float* __restrict__ out) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < m_pad; m += stride) {
-    if (m >= M || N == 0) { L[m] = 0.0f; continue; }
-    float best = -__builtin_inff();
-    for (int j = 0; j < samples; ++j) {
-      int64_t n = ((int64_t)j * N) / samples;
-      float dot = 0.0f;
-      for (int d = 0; d < D; ++d)
-        dot = fmaf(T::to_float(qs[rt_index(m, d, W)]), T::to_float(ks[rt_index(n, d, W)]), dot);
-      float x = tau2 * (dot + nhq[m] + nhk[n]);
-      best = fmaxf(best, x);
-    }
-    L[m] = best;
+  const float sc = slot ? ldexpf(1.0f, scale_exponent(*slot)) : 0.0f;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * 2; t += stride) {
+    const int64_t s = t >> 6;
+    const int i = (int)(t & 63);
+    const int64_t r = s * 32 + (i & 31);
+    float val;
+    if (i < 32)
+      val = nh[r];
+    else
+      val = (v && C == 1 && r < n) ? load_any(v, r, dtype) * sc : 0.0f;
+    out[t] = val;
   }
 }
 
