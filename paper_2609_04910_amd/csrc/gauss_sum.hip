@@ -65,23 +65,25 @@ using FwdFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint
                        const uint4*, const float*, const uint4*, const uint32_t*, float, int64_t, int,
                        int, int, float*, int64_t);
 
-template <typename T, int DP, int CT>
+template <typename T, int DP, int CT, bool ONE>
 void launch_fwd(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const uint4* srt,
                 const float* snh, const uint4* ks, const float* scal, const uint4* vt,
                 const uint32_t* vslot, float tau2, int64_t M, int C, int steps, int sps, float* out,
                 int64_t pstride) {
-  hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT)>), grid, dim3(kBlockThreads), 0, st, qs, nhq,
-                     srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride);
+  hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE>), grid, dim3(kBlockThreads), 0, st, qs,
+                     nhq, srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride);
 }
 
+// CT = 0 selects the single-channel form (one 16-row tile of signs).
 template <typename T, int DP>
 FwdFn fwd_by_ct(int CT) {
   switch (CT) {
-    case 1: return &launch_fwd<T, DP, 1>;
-    case 2: return &launch_fwd<T, DP, 2>;
-    case 4: return &launch_fwd<T, DP, 4>;
-    case 8: return &launch_fwd<T, DP, 8>;
-    case 16: return &launch_fwd<T, DP, 16>;
+    case 0: return &launch_fwd<T, DP, 1, true>;
+    case 1: return &launch_fwd<T, DP, 1, false>;
+    case 2: return &launch_fwd<T, DP, 2, false>;
+    case 4: return &launch_fwd<T, DP, 4, false>;
+    case 8: return &launch_fwd<T, DP, 8, false>;
+    case 16: return &launch_fwd<T, DP, 16, false>;
   }
   return nullptr;
 }
@@ -99,18 +101,18 @@ FwdFn fwd_fn(int DP, int CT) {
 
 using DqFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
                       const uint4*, const float*, const uint4*, const uint32_t*, const uint4*,
-                      const uint32_t*, const uint4*, const uint32_t*, float, float, int64_t, int, int,
-                      int, float*, int64_t);
+                      const uint32_t*, const uint4*, const uint32_t*, const void*, int, float, float,
+                      int64_t, int, int, int, float*, int64_t);
 
 template <typename T, int DP, int CW>
 void launch_dq(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const uint4* srt,
                const float* snh, const uint4* ks, const float* scal, const uint4* kt,
                const uint32_t* kslot, const uint4* vs, const uint32_t* vslot, const uint4* gsr,
-               const uint32_t* gslot, float tau2, float tau, int64_t M, int D, int steps, int sps,
-               float* out, int64_t pstride) {
+               const uint32_t* gslot, const void* g1, int g1_dtype, float tau2, float tau, int64_t M,
+               int D, int steps, int sps, float* out, int64_t pstride) {
   hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW)>), grid, dim3(kBlockThreads), 0, st, qs, nhq,
-                     srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, tau2, tau, M, D, steps, sps,
-                     out, pstride);
+                     srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, g1, g1_dtype, tau2, tau, M,
+                     D, steps, sps, out, pstride);
 }
 
 template <typename T, int DP>
@@ -152,7 +154,7 @@ struct Carver {
 struct Side {  // one point set with the arrays derived from it
   uint16_t* rt = nullptr;       // RT copy (input dtype)
   float* nh = nullptr;          // -||x||^2/2 (padding rows: kPadBias)
-  uint16_t* ks = nullptr;       // KS fp16 copy (operand of sum_n P k_n)
+  uint16_t* ks = nullptr;       // KS fp16 copy (operand of sum_n P k_n) as keys of a gradient pass
   uint16_t* samp_rt = nullptr;  // 64 sampled rows, RT layout
   float* samp_nh = nullptr;     // their half norms
 };
@@ -222,8 +224,11 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
     }
   };
   if (alias) {
+    // single channel: the KS copies carry the signs of v (dq) or dout (dk)
+    const bool two = p.C == 1 && need_q_ks && need_k_ks;
     side(pl.q, pl.Mp, need_q_ks || need_k_ks, true);
     pl.k = pl.q;
+    if (two) pl.k.ks = cv.take<uint16_t>(pl.Mp * W * 2);
   } else {
     side(pl.q, pl.Mp, need_q_ks, keys_q);
     side(pl.k, pl.Np, need_k_ks, keys_k);
@@ -293,9 +298,11 @@ struct Ctx {
   float tau, tau2;
 };
 
+// sgn / sgn_dt: for single-channel problems, the values whose signs the KS
+// copy of these points (as keys of a gradient pass) carries; else NULL.
 template <typename T>
 void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t n, int64_t n_pad, Side& s,
-                   uint32_t* slot) {
+                   uint32_t* slot, const void* sgn, gs_dtype sgn_dt) {
   const gs_problem& p = *c.p;
   const int W = c.pl->dm.W();
   hipLaunchKernelGGL(k_points_rt, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D, n_pad,
@@ -313,16 +320,32 @@ void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t n, int64_t n_pad, 
       sl = slot;
     }
     hipLaunchKernelGGL(k_points_ks<T>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
-                       n_pad, W, sl, s.ks);
+                       n_pad, W, sl, sgn, (int)sgn_dt, s.ks);
   }
 }
 
-void prep_points(const Ctx& c, const void* x, int64_t n, int64_t n_pad, Side& s, uint32_t* slot) {
+void prep_points(const Ctx& c, const void* x, int64_t n, int64_t n_pad, Side& s, uint32_t* slot,
+                 const void* sgn = nullptr, gs_dtype sgn_dt = GS_F32) {
   const uint16_t* x16 = static_cast<const uint16_t*>(x);
   if (c.p->qk_dtype == GS_F16)
-    prep_points_t<F16>(c, x16, n, n_pad, s, slot);
+    prep_points_t<F16>(c, x16, n, n_pad, s, slot, sgn, sgn_dt);
   else
-    prep_points_t<BF16>(c, x16, n, n_pad, s, slot);
+    prep_points_t<BF16>(c, x16, n, n_pad, s, slot, sgn, sgn_dt);
+}
+
+// KS copy only (the second, differently signed copy of aliased points).
+void prep_points_ks(const Ctx& c, const void* x, int64_t n, int64_t n_pad, uint16_t* ks,
+                    uint32_t* slot, const void* sgn, gs_dtype sgn_dt) {
+  const gs_problem& p = *c.p;
+  const int W = c.pl->dm.W();
+  const uint16_t* x16 = static_cast<const uint16_t*>(x);
+  const uint32_t* sl = p.qk_dtype == GS_BF16 ? slot : nullptr;
+  if (p.qk_dtype == GS_F16)
+    hipLaunchKernelGGL(k_points_ks<F16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
+                       n_pad, W, sl, sgn, (int)sgn_dt, ks);
+  else
+    hipLaunchKernelGGL(k_points_ks<BF16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n,
+                       (int)p.D, n_pad, W, sl, sgn, (int)sgn_dt, ks);
 }
 
 void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t n, int64_t n_pad, Vals& s,
@@ -337,16 +360,17 @@ void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t n, int64_t n_
                        (int)p.C, n_pad, Wv, (const uint32_t*)slot, s.rt);
   if (s.ks)
     hipLaunchKernelGGL(k_values_ks, dim3(grid1(n_pad * Rv)), dim3(256), 0, c.st, x, (int)dt, n,
-                       (int)p.C, n_pad, Rv, (const uint32_t*)slot, s.ks);
+                       (int)p.C, n_pad, Rv, (const uint32_t*)slot, (int)(p.C == 1), s.ks);
 }
 
 // Per-step key scalars of key side `s` paired with values x (slot = their
-// absolute maximum), for C = 1 gradient passes; half norms only otherwise.
+// absolute maximum): single-channel problems fold log2|v| and sign(v) in,
+// otherwise half norms only.
 void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64_t n, int64_t n_pad,
                   const uint32_t* slot, float* out) {
   const bool vals = c.p->C == 1 && x != nullptr;
   hipLaunchKernelGGL(k_step_scalars, dim3(grid1(n_pad * 2)), dim3(256), 0, c.st, (const float*)s.nh,
-                     vals ? x : nullptr, (int)dt, n, (int)c.p->C, n_pad, vals ? slot : nullptr, out);
+                     vals ? x : nullptr, (int)dt, n, n_pad, slot, c.tau2, out);
 }
 
 void combine(const Ctx& c, const PassShape& ps, int64_t count, float* out) {
@@ -361,7 +385,8 @@ void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t 
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
   PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT));
-  FwdFn fn = p.qk_dtype == GS_F16 ? fwd_fn<F16>(dm.DP, dm.CT) : fwd_fn<BF16>(dm.DP, dm.CT);
+  const int ct = p.C == 1 ? 0 : dm.CT;
+  FwdFn fn = p.qk_dtype == GS_F16 ? fwd_fn<F16>(dm.DP, ct) : fwd_fn<BF16>(dm.DP, ct);
   float* dst = ps.splits > 1 ? c.pl->part : out;
   prof_before(kKindFwd, c.st);
   fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
@@ -372,9 +397,11 @@ void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t 
 }
 
 // dq-type pass: out[m, :] = tau sum_n Phi(x_m, y_n) <gx_m, vy_n> (y_n - x_m).
+// g1 / g1_dt: the caller's single-channel upstream gradient of the query rows
+// (C = 1), read exactly in the epilogue.
 void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const float* scal,
              const uint32_t* kslot, const uint16_t* vrt, const uint32_t* vslot, const uint16_t* grt,
-             const uint32_t* gslot, float* out) {
+             const uint32_t* gslot, const void* g1, gs_dtype g1_dt, float* out) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
   const int cw = dq_cw(p, dm);
@@ -384,8 +411,8 @@ void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t n
   prof_before(kKindGrad, c.st);
   fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
      ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)ks.ks,
-     p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot, (const uint4*)grt, gslot,
-     c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst, ps.splits > 1 ? nq * p.D : 0);
+     p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot, (const uint4*)grt, gslot, g1,
+     (int)g1_dt, c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst, ps.splits > 1 ? nq * p.D : 0);
   prof_after(kKindGrad, c.st);
   combine(c, ps, nq * p.D, out);
 }
@@ -558,7 +585,7 @@ gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const
     prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2);
     if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3);
     prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
-    prep_scalars(c, pl.k, nullptr, p->v_dtype, N, pl.Np, nullptr, pl.scal_kv);
+    prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
     pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out);
     return launch_status();
   } catch (...) {
@@ -618,8 +645,18 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
 
     Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
     hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
-    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2);
-    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3);
+    const bool one = C == 1;
+    if (alias) {
+      // q.ks serves dk (keys q, signs of dout) unless only dq wants a KS copy
+      const bool q_for_dk = w.dk;
+      prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one ? (q_for_dk ? dout : v) : nullptr,
+                  q_for_dk ? dout_dtype : p->v_dtype);
+      if (pl.k.ks != pl.q.ks)
+        prep_points_ks(c, k, N, pl.Np, pl.k.ks, pl.slots + 2, v, p->v_dtype);
+    } else {
+      prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one ? dout : nullptr, dout_dtype);
+      prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, one ? v : nullptr, p->v_dtype);
+    }
     if (w.dq || w.dk) prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
     prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
     if (pl.scal_kv) prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
@@ -627,10 +664,10 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
     const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
     if (w.dq)
       pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1,
-              dq);
+              dout, dout_dtype, dq);
     if (w.dk)
       pass_dq(c, pl.k, N, pl.q, M, pl.scal_qg, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt,
-              pl.slots + 0, dk);
+              pl.slots + 0, v, p->v_dtype, dk);
     if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv);
     return launch_status();
   } catch (...) {

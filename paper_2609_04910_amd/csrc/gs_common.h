@@ -90,6 +90,13 @@ __device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, halfx2));
 }
 
+// Element i of an fp32 / fp16 / bf16 array (dtype codes of gs_dtype: 0, 1, 2).
+__device__ __forceinline__ float load_any(const void* p, int64_t i, int dtype) {
+  if (dtype == 0) return static_cast<const float*>(p)[i];
+  uint16_t b = static_cast<const uint16_t*>(p)[i];
+  return dtype == 1 ? F16::to_float(b) : BF16::to_float(b);
+}
+
 // Power-of-two scale exponent e with max * 2^e in [1, 2); 0 for max = 0, Inf or NaN.
 __device__ __forceinline__ int scale_exponent(uint32_t max_bits) {
   float mx = __builtin_bit_cast(float, max_bits);

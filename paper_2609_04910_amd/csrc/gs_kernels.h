@@ -7,10 +7,10 @@
 //          (k, v) exchanged, and k_fwd gives dv = sum_m Phi g_m likewise.
 //
 // Work decomposition: a workgroup is 4 waves that share one stream of key
-// steps (32 keys each) through LDS; wave w owns 16*QT queries whose operands
-// stay in registers.  Step s+1 is copied HBM -> LDS with the gfx950 direct
-// loads (global_load_lds_dwordx4, no register round trip) while step s is
-// computed, one barrier per step.  Per step and query tile a wave computes two
+// steps (32 keys each) through a three-stage LDS ring; wave w owns 16*QT
+// queries whose operands stay in registers.  Step s+2 is copied HBM -> LDS
+// with the gfx950 direct loads (global_load_lds_dwordx4, no register round
+// trip) while step s is computed, one barrier per step.  Per step and query tile a wave computes two
 // 16x16 tiles of S~^T[n][m] = q_m.k_n - ||k_n||^2/2 on the matrix cores (the
 // key half-norm enters as the accumulator input, so it costs no vector
 // instruction), forms the exponent x = tau' S~ + (-tau'||q_m||^2/2 - off_m)
@@ -42,17 +42,73 @@ constexpr int kScalarFloats = 64;      // per step: 32 half norms, 32 scaled C =
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void glb_void;
 
-// One wave copies 1 KiB: lane l moves 16 bytes from src + 16 l to dst + 16 l.
-__device__ __forceinline__ void dma_1k(const char* src, char* dst, int lane) {
-  __builtin_amdgcn_global_load_lds((glb_void*)(src + 16 * lane), (lds_void*)dst, 16, 0, 0);
+// Buffer resource over `bytes` bytes from `base` (raw, unswizzled; reads past
+// the end return zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
 }
-// One wave copies 256 bytes: lane l moves 4 bytes.
-__device__ __forceinline__ void dma_256(const char* src, char* dst, int lane) {
-  __builtin_amdgcn_global_load_lds((glb_void*)(src + 4 * lane), (lds_void*)dst, 4, 0, 0);
+
+// Direct HBM -> LDS copies (buffer_load ... lds): lane l moves `size` bytes
+// from rsrc + voff + soff to LDS address m0 + size * l.  They are issued as
+// inline assembly so that the compiler neither sees nor waits for the
+// asynchronous LDS writes; the key stream below orders them explicitly
+// (s_waitcnt vmcnt + s_barrier).  Every wave issues one load per 1-KiB chunk of
+// a step, moving its quarter of it (lanes 16w .. 16w+15, 16 bytes each), and
+// one dword load for its quarter of the 256 bytes of step scalars, so all
+// waves issue the same number of loads per step and "step s has landed" is an
+// exact vmcnt.  Addresses are a buffer resource (SGPRs), a per-lane VGPR
+// offset fixed for the kernel and a per-step SGPR offset.
+__device__ __forceinline__ void dma_x4(__amdgpu_buffer_rsrc_t rs, uint32_t soff, uint32_t lds,
+                                       uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rs), "s"(soff)
+               : "memory", "m0");
 }
-// Wait until this wave's outstanding vector-memory loads (including the
-// direct-to-LDS ones) have landed.
-__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+__device__ __forceinline__ void dma_x1(__amdgpu_buffer_rsrc_t rs, uint32_t soff, uint32_t lds,
+                                       uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rs), "s"(soff)
+               : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(N), as assembly so that it is kept exactly as written.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)(const lds_void*)p;
+}
+
+// Three-stage LDS ring over the key steps [s_begin, s_end): step s+2 streams
+// in while step s is computed, with one barrier per step.  issue(s, k)
+// enqueues the NL loads of step s into stage k; compute(k) consumes stage k.
+template <int NL, typename Issue, typename Compute>
+__device__ __forceinline__ void key_stream(int s_begin, int s_end, Issue issue, Compute compute) {
+  if (s_begin < s_end) issue(s_begin, 0);
+  if (s_begin + 1 < s_end) issue(s_begin + 1, 1);
+  int cur = 0;
+  for (int s = s_begin; s < s_end; ++s) {
+    if (s + 1 < s_end)
+      wait_vmcnt<NL>();  // only step s+1 may still be in flight
+    else
+      wait_vmcnt<0>();
+    // After the barrier step s is visible to all waves and the stage read in
+    // step s-1 is free; the empty assembly keeps the compiler from moving
+    // memory accesses across it.
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (s + 2 < s_end) issue(s + 2, cur == 0 ? 2 : cur - 1);
+    compute(cur);
+    cur = cur == 2 ? 0 : cur + 1;
+  }
+}
 
 __device__ __forceinline__ float max4(floatx4 a) {
   return fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3]));
@@ -136,6 +192,15 @@ __device__ __forceinline__ void exact_offsets(const uint4* __restrict__ ks, cons
   }
 }
 
+// acc + sum over the 8 fp16 products a_i b_i (v_dot2_f32_f16, fp32 accumulation).
+__device__ __forceinline__ float dot2_acc(uint4 a, uint4 b, float acc) {
+  acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(halfx2, a.x), __builtin_bit_cast(halfx2, b.x), acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(halfx2, a.y), __builtin_bit_cast(halfx2, b.y), acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(halfx2, a.z), __builtin_bit_cast(halfx2, b.z), acc, false);
+  acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(halfx2, a.w), __builtin_bit_cast(halfx2, b.w), acc, false);
+  return acc;
+}
+
 __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
   uint4 b;
   b.x = pack_f16(p[0][0], p[0][1]);
@@ -147,7 +212,10 @@ __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
 
 // ---------------------------------------------------------------- forward
 
-template <typename T, int DP, int CT, int QT>
+// ONE (single channel, C = 1): the magnitude of v_n enters the exponent via the
+// step scalars (log2 |v_n 2^e| added to the key bias, max |v 2^e| in
+// [0.5, 1)) and V^T holds only the signs, so v contributes no fp16 rounding.
+template <typename T, int DP, int CT, int QT, bool ONE>
 __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
@@ -156,7 +224,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
   constexpr int KCH = 2 * DP;   // 1-KiB chunks of keys per step
   constexpr int NCH = KCH + CT; // + chunks of V^T
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
-  __shared__ __attribute__((aligned(1024))) char lds[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char lds[3 * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -166,17 +234,25 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
   const int s_end = min(steps_total, s_begin + steps_per_split);
   out += blockIdx.y * part_stride;
 
+  const bool mine = g == wave;
+  // buffer resources over this split's part of each key-side stream
+  const uint32_t nsteps = (uint32_t)max(0, s_end - s_begin);
+  const auto rk = make_rsrc(reinterpret_cast<const char*>(ks) + (int64_t)s_begin * KCH * 1024,
+                            nsteps * KCH * 1024);
+  const auto rv = make_rsrc(reinterpret_cast<const char*>(vt) + (int64_t)s_begin * CT * 1024,
+                            nsteps * CT * 1024);
+  const auto rsc = make_rsrc(scal + (int64_t)s_begin * kScalarFloats, nsteps * kScalarFloats * 4);
+  const uint32_t lds0 = lds_address(lds);
   auto issue = [&](int s, int stage) {
-    char* base = lds + stage * STAGE;
-    for (int c = wave; c < NCH; c += kWavesPerBlock) {
-      const char* src = c < KCH ? reinterpret_cast<const char*>(ks) + ((int64_t)s * KCH + c) * 1024
-                                : reinterpret_cast<const char*>(vt) + ((int64_t)s * CT + (c - KCH)) * 1024;
-      dma_1k(src, base + c * 1024, lane);
-    }
-    if (wave == kWavesPerBlock - 1)
-      dma_256(reinterpret_cast<const char*>(scal + (int64_t)s * kScalarFloats), base + NCH * 1024, lane);
+    if (!mine) return;
+    const uint32_t base = lds0 + stage * STAGE;
+    const uint32_t ls = (uint32_t)(s - s_begin);
+#pragma unroll
+    for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+#pragma unroll
+    for (int c = 0; c < CT; ++c) dma_x4(rv, (ls * CT + c) * 1024, base + (KCH + c) * 1024, 16 * lane);
+    dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
   };
-  if (s_begin < s_end) issue(s_begin, 0);
 
   uint4 qreg[QT][DP];
   float bq[QT], off[QT];
@@ -195,11 +271,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) O[qt][ct] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  for (int s = s_begin; s < s_end; ++s) {
-    const int stage = (s - s_begin) & 1;
-    wait_loads();
-    __syncthreads();
-    if (s + 1 < s_end) issue(s + 1, stage ^ 1);
+  auto compute = [&](int stage) {
     const char* base = lds + stage * STAGE;
     const uint4* kb = reinterpret_cast<const uint4*>(base);
     const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
@@ -227,9 +299,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) O[qt][ct] = mfma_f16(vr[ct], b, O[qt][ct]);
     }
-  }
+  };
+  key_stream<NCH + 1>(s_begin, s_end, issue, compute);
 
-  const int ev = scale_exponent(*vslot);
+  const int ev = scale_exponent(*vslot) - (ONE ? 1 : 0);
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int64_t m = q0 + 16 * qt + j;
@@ -247,9 +320,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 
 // ---------------------------------------------------------------- gradient
 //
-// CW = 0 selects the single-channel form (C = 1): w_mn = g_m v_n, so
-// P = Phi v_n uses the per-key scaled values from the step scalars (one
-// v_mul per pair, no W contraction) and g_m multiplies the epilogue.
+// CW = 0 selects the single-channel form (C = 1): w_mn = g_m v_n.  |v_n|
+// enters the exponent through the step scalars (as in k_fwd), sign(v_n) is
+// folded into the KS copy of the keys, so P' = |Phi v_n| needs no multiply and
+// no W contraction; the row sums take the signs from the step scalars, and
+// g_m (exact, from the caller's array) multiplies the epilogue.  Row sums
+// sum_n P use v_dot2_f32_f16 on the same fp16 values the dQ MFMA consumes.
 
 template <typename T, int DP, int CW, int QT>
 __global__ __launch_bounds__(kBlockThreads) void k_dq(
@@ -257,8 +333,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
     const uint4* __restrict__ kt_ks, const uint32_t* __restrict__ kslot, const uint4* __restrict__ vs,
     const uint32_t* __restrict__ vslot, const uint4* __restrict__ gs,
-    const uint32_t* __restrict__ gslot, float tau2, float tau, int64_t M, int D, int steps_total,
-    int steps_per_split, float* __restrict__ out, int64_t part_stride) {
+    const uint32_t* __restrict__ gslot, const void* __restrict__ g1, int g1_dtype, float tau2,
+    float tau, int64_t M, int D, int steps_total, int steps_per_split, float* __restrict__ out,
+    int64_t part_stride) {
   constexpr int DT = 2 * DP;                // 16-row tiles of K^T (KS layout)
   constexpr int KCH = 2 * DP;               // chunks of K (RT) per step
   constexpr int VCH = 2 * CW;               // chunks of V (RT) per step
@@ -266,7 +343,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
   constexpr int NCH = KCH + VCH + TCH;
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
   constexpr int GW = CW > 0 ? CW : 1;       // RT chunks of the upstream gradient
-  __shared__ __attribute__((aligned(1024))) char lds[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char lds[3 * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -276,22 +353,30 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
   const int s_end = min(steps_total, s_begin + steps_per_split);
   out += blockIdx.y * part_stride;
 
+  const bool mine = g == wave;
+  // buffer resources over this split's part of each key-side stream
+  const uint32_t nsteps = (uint32_t)max(0, s_end - s_begin);
+  const auto rk = make_rsrc(reinterpret_cast<const char*>(ks) + (int64_t)s_begin * KCH * 1024,
+                            nsteps * KCH * 1024);
+  const auto rv = make_rsrc(reinterpret_cast<const char*>(vs) + (int64_t)s_begin * VCH * 1024,
+                            nsteps * VCH * 1024);
+  const auto rt = make_rsrc(reinterpret_cast<const char*>(kt_ks) + (int64_t)s_begin * TCH * 1024,
+                            nsteps * TCH * 1024);
+  const auto rsc = make_rsrc(scal + (int64_t)s_begin * kScalarFloats, nsteps * kScalarFloats * 4);
+  const uint32_t lds0 = lds_address(lds);
   auto issue = [&](int s, int stage) {
-    char* base = lds + stage * STAGE;
-    for (int c = wave; c < NCH; c += kWavesPerBlock) {
-      const char* src;
-      if (c < KCH)
-        src = reinterpret_cast<const char*>(ks) + ((int64_t)s * KCH + c) * 1024;
-      else if (c < KCH + VCH)
-        src = reinterpret_cast<const char*>(vs) + ((int64_t)s * VCH + (c - KCH)) * 1024;
-      else
-        src = reinterpret_cast<const char*>(kt_ks) + ((int64_t)s * TCH + (c - KCH - VCH)) * 1024;
-      dma_1k(src, base + c * 1024, lane);
-    }
-    if (wave == kWavesPerBlock - 1)
-      dma_256(reinterpret_cast<const char*>(scal + (int64_t)s * kScalarFloats), base + NCH * 1024, lane);
+    if (!mine) return;
+    const uint32_t base = lds0 + stage * STAGE;
+    const uint32_t ls = (uint32_t)(s - s_begin);
+#pragma unroll
+    for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+#pragma unroll
+    for (int c = 0; c < VCH; ++c) dma_x4(rv, (ls * VCH + c) * 1024, base + (KCH + c) * 1024, 16 * lane);
+#pragma unroll
+    for (int c = 0; c < TCH; ++c)
+      dma_x4(rt, (ls * TCH + c) * 1024, base + (KCH + VCH + c) * 1024, 16 * lane);
+    dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
   };
-  if (s_begin < s_end) issue(s_begin, 0);
 
   uint4 qreg[QT][DP];
   uint4 greg[QT][GW];
@@ -307,37 +392,32 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
     exact_offsets<T, DP, QT>(ks, scal, qreg, s_begin, s_end, j, g, tau2, bq, off);
 
   floatx4 dQ[QT][DT];
-  floatx4 rs[QT];
+  float rs[QT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    rs[qt] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    rs[qt] = 0.0f;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) dQ[qt][dt] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
   }
-  const uint4 ones = {0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};  // fp16 1.0
 
-  for (int s = s_begin; s < s_end; ++s) {
-    const int stage = (s - s_begin) & 1;
-    wait_loads();
-    __syncthreads();
-    if (s + 1 < s_end) issue(s + 1, stage ^ 1);
+  auto compute = [&](int stage) {
     const char* base = lds + stage * STAGE;
     const uint4* kb = reinterpret_cast<const uint4*>(base);
     const uint4* vb = reinterpret_cast<const uint4*>(base + KCH * 1024);
     const uint4* tb = reinterpret_cast<const uint4*>(base + (KCH + VCH) * 1024);
     const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
-    floatx4 cin[2], vv[2];
+    floatx4 cin[2];
     uint4 kr[2][DP];
     uint4 vr[2][GW];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
       load_k_tile<DP>(kb, kt, j, g, kr[kt]);
-      if constexpr (CW > 0)
-        load_k_tile<GW>(vb, kt, j, g, vr[kt]);
-      else
-        vv[kt] = *reinterpret_cast<const floatx4*>(sc + 32 + 16 * kt + 4 * g);
+      if constexpr (CW > 0) load_k_tile<GW>(vb, kt, j, g, vr[kt]);
     }
+    // per key slot of this lane's B operand: sign(v_n) (single channel) or 1
+    const uint4 sg = CW > 0 ? uint4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u}
+                            : *reinterpret_cast<const uint4*>(sc + 32 + 4 * g);
     uint4 ktr[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + j) * 4 + g];
@@ -347,43 +427,47 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         const floatx4 acc = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
-        floatx4 w;
         if constexpr (CW > 0) {
-          w = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+          floatx4 w = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
           for (int cw = 0; cw < CW; ++cw) w = mfma_f16(vr[kt][cw], greg[qt][cw], w);
-        } else {
-          w = vv[kt];
-        }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[r], tau2, bq[qt])) * w[r];
+          for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[r], tau2, bq[qt])) * w[r];
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[r], tau2, bq[qt]));
+        }
       }
       const uint4 b = pack_tile_pair(p);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) dQ[qt][dt] = mfma_f16(ktr[dt], b, dQ[qt][dt]);
-      rs[qt] = mfma_f16(ones, b, rs[qt]);
+      rs[qt] = dot2_acc(b, sg, rs[qt]);
     }
-  }
+  };
+  key_stream<NCH + 1>(s_begin, s_end, issue, compute);
 
-  const int ev = scale_exponent(*vslot);
-  const int eg = scale_exponent(*gslot);
   const int ek = kslot ? scale_exponent(*kslot) : 0;
   const uint16_t* q16 = reinterpret_cast<const uint16_t*>(qs);
-  const uint16_t* g16 = reinterpret_cast<const uint16_t*>(gs);
+  // rs holds this lane's 8-key partial sums; add the other three key groups
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    rs[qt] += __shfl_xor(rs[qt], 16, kWave);
+    rs[qt] += __shfl_xor(rs[qt], 32, kWave);
+  }
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int64_t m = q0 + 16 * qt + j;
     if (m >= M) continue;
     float f = tau * exp2f(off[qt]);
-    int e = -ev;
+    int e;
     if constexpr (CW > 0) {
-      e -= eg;
+      e = -scale_exponent(*vslot) - scale_exponent(*gslot);
     } else {
-      // single channel: w = g_m v_n, with g_m from its scaled fp16 copy
-      f *= (float)__builtin_bit_cast(_Float16, g16[rt_index(m, 0, 32)]);
-      e -= eg;
+      // single channel: w = g_m v_n with v_n 2^(ev-1) in the kernel values
+      e = 1 - scale_exponent(*vslot);
+      f *= load_any(g1, m, g1_dtype);
     }
-    const float rm = rs[qt][0];
+    const float rm = rs[qt];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll

@@ -26,12 +26,6 @@ __global__ void k_fill_f32(float* __restrict__ p, int64_t n, float val) {
   for (; i < n; i += stride) p[i] = val;
 }
 
-// dtype codes follow gs_dtype: 0 = fp32, 1 = fp16, 2 = bf16.
-__device__ __forceinline__ float load_any(const void* p, int64_t i, int dtype) {
-  if (dtype == 0) return static_cast<const float*>(p)[i];
-  uint16_t b = static_cast<const uint16_t*>(p)[i];
-  return dtype == 1 ? F16::to_float(b) : BF16::to_float(b);
-}
 
 // max |x| over count elements into *slot (float bits; |x| >= 0 so unsigned
 // comparison of the bit patterns orders them; NaN compares largest).
@@ -81,12 +75,16 @@ __global__ void k_points_norm(const uint16_t* __restrict__ x, int64_t n, int D, 
   }
 }
 
+
 // Points, KS-layout fp16 copy scaled by 2^e (e from *slot when slot != NULL,
-// needed for bf16 inputs whose range exceeds fp16).  One thread per element,
-// keys fastest so that the writes of a wave stay within a few 64-byte lines.
+// needed for bf16 inputs whose range exceeds fp16) and, when sgn != NULL,
+// multiplied by the sign of the single-channel value sgn[r] (exact).  One
+// thread per element, keys fastest so that the writes of a wave stay within a
+// few 64-byte lines.
 template <typename T>
 __global__ void k_points_ks(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad, int R,
-                            const uint32_t* __restrict__ slot, uint16_t* __restrict__ xt) {
+                            const uint32_t* __restrict__ slot, const void* __restrict__ sgn,
+                            int sgn_dtype, uint16_t* __restrict__ xt) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float s = slot ? ldexpf(1.0f, scale_exponent(*slot)) : 1.0f;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * R; t += stride) {
@@ -95,6 +93,7 @@ __global__ void k_points_ks(const uint16_t* __restrict__ x, int64_t n, int D, in
     int w = rem >> 5;
     int64_t r = blk * 32 + (rem & 31);
     float v = (r < n && w < D) ? T::to_float(x[r * D + w]) * s : 0.0f;
+    if (sgn && r < n && load_any(sgn, r, sgn_dtype) < 0.0f) v = -v;
     _Float16 h = (_Float16)v;
     xt[ks_index(r, w, R)] = __builtin_bit_cast(uint16_t, h);
   }
@@ -115,8 +114,11 @@ __global__ void k_values_rt(const void* __restrict__ v, int dtype, int64_t n, in
   }
 }
 
+// With sign_only (single-channel values, whose magnitudes enter the exponent
+// through the step scalars) row 0 holds sign(v) = +-1 instead.
 __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, int C, int64_t n_pad,
-                            int R, const uint32_t* __restrict__ slot, uint16_t* __restrict__ vt) {
+                            int R, const uint32_t* __restrict__ slot, int sign_only,
+                            uint16_t* __restrict__ vt) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float s = ldexpf(1.0f, scale_exponent(*slot));
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * R; t += stride) {
@@ -125,6 +127,7 @@ __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, in
     int w = rem >> 5;
     int64_t r = blk * 32 + (rem & 31);
     float val = (r < n && w < C) ? load_any(v, r * C + w, dtype) * s : 0.0f;
+    if (sign_only) val = (r < n && w == 0) ? (val < 0.0f ? -1.0f : 1.0f) : 0.0f;
     _Float16 h = (_Float16)val;
     vt[ks_index(r, w, R)] = __builtin_bit_cast(uint16_t, h);
   }
@@ -153,22 +156,38 @@ __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W
   }
 }
 
-// Per-step key scalars: for step s, 32 half norms followed by 32 scaled
-// single-channel values (v * 2^e, e from *slot; zeros when C > 1 or no values).
+// Per-step key scalars, 64 floats (256 bytes) per 32-key step:
+//   [0, 32)  key bias b_n = -||k_n||^2/2, and for single-channel values
+//            (v != NULL) additionally log2|v_n 2^e| / tau' with e from *slot
+//            putting max |v 2^e| in [0.5, 1): the magnitude of v_n then enters
+//            the exponent in fp32 (log2 0 = -inf gives an exact 0);
+//   [32, 48) for single-channel values, sign(v_n) as fp16 +-1 in key-slot
+//            order (the order of the MFMA B operand built from two score
+//            tiles), two per float; otherwise 0;
+//   [48, 64) unused, 0.
 __global__ void k_step_scalars(const float* __restrict__ nh, const void* __restrict__ v, int dtype,
-                               int64_t n, int C, int64_t n_pad, const uint32_t* __restrict__ slot,
+                               int64_t n, int64_t n_pad, const uint32_t* __restrict__ slot, float tau2,
                                float* __restrict__ out) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const float sc = slot ? ldexpf(1.0f, scale_exponent(*slot)) : 0.0f;
+  const float sc = v ? ldexpf(1.0f, scale_exponent(*slot) - 1) : 0.0f;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * 2; t += stride) {
     const int64_t s = t >> 6;
     const int i = (int)(t & 63);
-    const int64_t r = s * 32 + (i & 31);
-    float val;
-    if (i < 32)
+    float val = 0.0f;
+    if (i < 32) {
+      const int64_t r = s * 32 + i;
       val = nh[r];
-    else
-      val = (v && C == 1 && r < n) ? load_any(v, r, dtype) * sc : 0.0f;
+      if (v && r < n) val += log2f(fabsf(load_any(v, r, dtype) * sc)) / tau2;
+    } else if (i < 48 && v) {
+      uint32_t bits = 0;
+      for (int h = 0; h < 2; ++h) {
+        const int z = 2 * (i - 32) + h;
+        const int64_t r = s * 32 + 16 * ((z & 7) >> 2) + 4 * (z >> 3) + (z & 3);
+        const bool neg = r < n && load_any(v, r, dtype) < 0.0f;
+        bits |= (neg ? 0xBC00u : 0x3C00u) << (16 * h);
+      }
+      val = __builtin_bit_cast(float, bits);
+    }
     out[t] = val;
   }
 }
