@@ -5,7 +5,9 @@ Default workload (one "step" = the whole hot path over one batch):
   Gaussian clouds, means 0 and 0.5*1, fp16), signed two-sample weights
   v = +-1/N (C = 1), tau = 1/median squared pairwise distance; a step is the
   forward sum s = sum_n Phi v_n plus its query gradient dq (upstream gradient
-  g = v), i.e. what one MMD-flow iteration evaluates.
+  g = v), i.e. what one MMD-flow iteration evaluates.  By default a step is
+  one gauss_sum_fwd_bwd call (the forward and dq from one pass over the pairs);
+  --separate times gauss_sum_fwd followed by gauss_sum_bwd instead.
 
 Other workloads (--workload) use the same JSON format: dense_d16 (forward),
 svgd (forward + dq, dk, dv), mixture_d32 (forward, --tau), rect_d256
@@ -42,12 +44,18 @@ PASSES = {
 }
 
 
-def flops_per_pair(passes, D, C):
+def flops_per_pair(passes, D, C, fused):
     """Algorithmic flops per (query, key) pair: the matrix contractions of each
     pass (q.k, the value or gradient contraction and, for gradients, the sum
-    over keys of P k), no padding or recomputation counted."""
+    over keys of P k), no padding or recomputation counted.  A fused forward +
+    dq pass computes q.k once: 2D (q.k) + 2C (values) + 2C (w) + 2D (P k)."""
     f = 0
-    for p in passes:
+    ps = list(passes)
+    if fused and "fwd" in ps and "dq" in ps:
+        f += 4 * D + 4 * C
+        ps.remove("fwd")
+        ps.remove("dq")
+    for p in ps:
         if p in ("fwd", "dv"):
             f += 2 * D + 2 * C
         else:  # dq or dk
@@ -85,7 +93,9 @@ def cpu_baseline(w, passes, budget_s=15.0):
                 oracle.dv(w.q_values, w.k_values, w.v, g, float(w.tau), rows=rows_k, threads=threads)
         return time.perf_counter() - t0
 
-    # calibrate on a few rows, then size the sample to about budget_s seconds
+    # warm up (library load, thread start), calibrate on a few rows, then size
+    # the sample to about budget_s seconds
+    run(np.arange(1), np.arange(1))
     nq = min(w.M, max(threads, 16))
     nk = min(w.N, max(1, int(nq * w.M / max(w.N, 1)) or 1))
     t = run(np.arange(nq), np.arange(nk))
@@ -123,6 +133,9 @@ def main():
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--separate", action="store_true",
+                    help="time separate gauss_sum_fwd + gauss_sum_bwd calls instead of one "
+                         "gauss_sum_fwd_bwd call")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -160,15 +173,21 @@ def main():
     g = t(w.g) if w.g is not None else None
     grads = tuple(p in passes for p in ("dq", "dk", "dv"))
     do_fwd = "fwd" in passes
+    fused = do_fwd and any(grads) and not args.separate
     qk_code = gs.GS_F16 if w.qk_dtype == "f16" else gs.GS_BF16
     v_code = {np.dtype(np.float32): gs.GS_F32, np.dtype(np.float16): gs.GS_F16}[w.v.dtype]
     ws_f = gs.gauss_sum_fwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code) if do_fwd else 0
     ws_b = gs.gauss_sum_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if any(grads) else 0
-    ws = torch.empty(max(ws_f, ws_b, 1), dtype=torch.uint8, device=dev)
+    ws_fb = gs.gauss_sum_fwd_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if fused else 0
+    ws = torch.empty(max(ws_f, ws_b, ws_fb, 1), dtype=torch.uint8, device=dev)
     out = torch.empty((w.M, w.C), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
+        if fused:
+            gs.gauss_sum_fwd_bwd(q, k, v, float(w.tau), g, want=grads, out=out, workspace=ws,
+                                 stream=stream)
+            return
         if do_fwd:
             gs.gauss_sum_fwd(q, k, v, float(w.tau), out=out, workspace=ws, stream=stream)
         if any(grads):
@@ -196,12 +215,22 @@ def main():
     pairs = float(w.M) * float(w.N)
     value = pairs / (ms_per_step * 1e-3)
 
-    # dominant kernel: the gradient kernel when gradients are taken, else the
-    # forward kernel; one launch processes M*N pairs
-    dom_flops = (4 * w.D + 2 * w.C if any(grads) else 2 * w.D + 2 * w.C) * pairs
+    # dominant kernel: the gradient kernel when gradients are taken (with the
+    # forward sum fused into the dq launch by default), else the forward
+    # kernel; one launch processes M*N pairs.  With dk also taken the launches
+    # alternate dq (fused) and dk; the per-launch work is averaged.
+    if any(grads):
+        per_launch = []
+        if grads[0]:
+            per_launch.append(4 * w.D + (4 if fused else 2) * w.C)
+        if grads[1]:
+            per_launch.append(4 * w.D + 2 * w.C)
+        dom_flops = float(np.mean(per_launch)) * pairs
+    else:
+        dom_flops = (2 * w.D + 2 * w.C) * pairs
     avg_kernel_ms = float(np.mean(kernel_ms)) if kernel_ms else float("nan")
     achieved = dom_flops / (avg_kernel_ms * 1e-3) / 1e12
-    step_flops = flops_per_pair(passes, w.D, w.C) * pairs
+    step_flops = flops_per_pair(passes, w.D, w.C, fused) * pairs
 
     res = {
         "metric": METRIC,
@@ -217,11 +246,14 @@ def main():
         "dtype": "f16" if w.qk_dtype == "f16" else "bf16",
         "data": "synthetic",
         "config": {"workload": describe(w, passes), "M": w.M, "N": w.N, "D": w.D, "C": w.C,
-                   "tau": float(w.tau), "passes": "+".join(passes)},
+                   "tau": float(w.tau), "passes": "+".join(passes),
+                   "api": "gauss_sum_fwd_bwd" if fused else
+                          "+".join(n for n, u in (("gauss_sum_fwd", do_fwd),
+                                                  ("gauss_sum_bwd", any(grads))) if u)},
         "mfma_frac_of_peak": step_flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
         "roofline": {
             "bound": "mfma",
-            "kernel": "k_dq" if any(grads) else "k_fwd",
+            "kernel": ("k_dq (forward fused)" if fused else "k_dq") if any(grads) else "k_fwd",
             "achieved": achieved,
             "peak": PEAK_MFMA_F16 / 1e12,
             "unit": "TFLOP/s",

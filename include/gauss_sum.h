@@ -107,6 +107,23 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
                         const void* dout, gs_dtype dout_dtype, float* dq, float* dk, float* dv,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Forward and backward in one call: writes out (as gauss_sum_fwd, required)
+ * and any of dq, dk, dv (as gauss_sum_bwd, NULL = not requested) for the
+ * given upstream gradient dout.  Sec. 3 of the paper observes that the query
+ * gradient is itself one kernel sum over the same pairs (values (v_n k_n,
+ * v_n)); with dq requested, the forward sum is produced by the same pass that
+ * computes dq, so the kernel values are evaluated once for both.  Meant for
+ * callers that know dout before the forward result (MMD flows use dout = v).
+ * Results equal those of separate gauss_sum_fwd and gauss_sum_bwd calls to
+ * within the stated tolerance. */
+gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, const void* v,
+                            float tau, const void* dout, gs_dtype dout_dtype, float* out, float* dq,
+                            float* dk, float* dv, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/* Bytes of device workspace gauss_sum_fwd_bwd needs (0 if p is invalid). */
+size_t gauss_sum_fwd_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv);
+
 /* Static, never-NULL description of a status code. */
 const char* gauss_sum_status_string(gs_status s);
 

@@ -102,38 +102,45 @@ FwdFn fwd_fn(int DP, int CT) {
 using DqFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
                       const uint4*, const float*, const uint4*, const uint32_t*, const uint4*,
                       const uint32_t*, const uint4*, const uint32_t*, const void*, int, float, float,
-                      int64_t, int, int, int, float*, int64_t);
+                      int64_t, int, int, int, float*, int64_t, const uint4*, int, float*, int64_t);
 
-template <typename T, int DP, int CW>
+template <typename T, int DP, int CW, int FCT>
 void launch_dq(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const uint4* srt,
                const float* snh, const uint4* ks, const float* scal, const uint4* kt,
                const uint32_t* kslot, const uint4* vs, const uint32_t* vslot, const uint4* gsr,
                const uint32_t* gslot, const void* g1, int g1_dtype, float tau2, float tau, int64_t M,
-               int D, int steps, int sps, float* out, int64_t pstride) {
-  hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW)>), grid, dim3(kBlockThreads), 0, st, qs, nhq,
+               int D, int steps, int sps, float* out, int64_t pstride, const uint4* vt, int C,
+               float* out_s, int64_t pstride_s) {
+  hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT>), grid, dim3(kBlockThreads), 0, st, qs, nhq,
                      srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, g1, g1_dtype, tau2, tau, M,
-                     D, steps, sps, out, pstride);
+                     D, steps, sps, out, pstride, vt, C, out_s, pstride_s);
+}
+
+// fused: also produce the forward sum (FCT = 1 for C = 1, else the V^T tiles).
+template <typename T, int DP, int CW, int CTF>
+DqFn dq_pick(bool fused) {
+  return fused ? &launch_dq<T, DP, CW, CTF> : &launch_dq<T, DP, CW, 0>;
 }
 
 template <typename T, int DP>
-DqFn dq_by_cw(int CW) {
+DqFn dq_by_cw(int CW, int CT, bool fused) {
   switch (CW) {
-    case 0: return &launch_dq<T, DP, 0>;
-    case 1: return &launch_dq<T, DP, 1>;
-    case 2: return &launch_dq<T, DP, 2>;
-    case 4: return &launch_dq<T, DP, 4>;
-    case 8: return &launch_dq<T, DP, 8>;
+    case 0: return dq_pick<T, DP, 0, 1>(fused);
+    case 1: return CT == 2 ? dq_pick<T, DP, 1, 2>(fused) : dq_pick<T, DP, 1, 1>(fused);
+    case 2: return dq_pick<T, DP, 2, 4>(fused);
+    case 4: return dq_pick<T, DP, 4, 8>(fused);
+    case 8: return dq_pick<T, DP, 8, 16>(fused);
   }
   return nullptr;
 }
 
 template <typename T>
-DqFn dq_fn(int DP, int CW) {
+DqFn dq_fn(int DP, int CW, int CT, bool fused) {
   switch (DP) {
-    case 1: return dq_by_cw<T, 1>(CW);
-    case 2: return dq_by_cw<T, 2>(CW);
-    case 4: return dq_by_cw<T, 4>(CW);
-    case 8: return dq_by_cw<T, 8>(CW);
+    case 1: return dq_by_cw<T, 1>(CW, CT, fused);
+    case 2: return dq_by_cw<T, 2>(CW, CT, fused);
+    case 4: return dq_by_cw<T, 4>(CW, CT, fused);
+    case 8: return dq_by_cw<T, 8>(CW, CT, fused);
   }
   return nullptr;
 }
@@ -173,8 +180,8 @@ struct Plan {
   Vals v, g;
   float* scal_kv = nullptr;    // per-step scalars, keys k with values v
   float* scal_qg = nullptr;    // per-step scalars, keys q with values dout
-  float* part = nullptr;
-  size_t part_bytes = 0;
+  float* part = nullptr;       // split partials of the running pass
+  float* part_s = nullptr;     // split partials of a forward sum fused into the dq pass
   size_t total = 0;
 };
 
@@ -196,6 +203,7 @@ PassShape pass_shape(int64_t rows, int64_t keys, int QT) {
 
 struct Want {
   bool fwd = false, dq = false, dk = false, dv = false;
+  bool fused() const { return fwd && dq; }  // forward computed inside the dq pass
 };
 
 inline int dq_cw(const gs_problem& p, const Dims& dm) { return p.C == 1 ? 0 : dm.CW; }
@@ -236,23 +244,27 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   if (keys_k) pl.scal_kv = cv.take<float>(pl.Np * 2 * 4);
   if (keys_q) pl.scal_qg = cv.take<float>(pl.Mp * 2 * 4);
   if (w.dq || w.dk) pl.v.rt = cv.take<uint16_t>(pl.Np * Wv * 2);
-  if (w.fwd) pl.v.ks = cv.take<uint16_t>(pl.Np * Rv * 2);
+  if (w.fwd && !(w.fused() && p.C == 1)) pl.v.ks = cv.take<uint16_t>(pl.Np * Rv * 2);
   if (w.dq || w.dk) pl.g.rt = cv.take<uint16_t>(pl.Mp * Wv * 2);
   if (w.dv) pl.g.ks = cv.take<uint16_t>(pl.Mp * Rv * 2);
 
   // Partial-sum buffer for split passes (reused by every pass in turn).
-  size_t part = 0;
+  size_t part = 0, part_s = 0;
   auto consider = [&](int64_t rows, int64_t keys, int QT, int64_t width) {
     PassShape ps = pass_shape(rows, keys, QT);
     if (ps.splits > 1) part = std::max(part, (size_t)ps.splits * rows * width * 4);
+    return ps.splits;
   };
   const int qf = fwd_qt(pl.dm.DP, pl.dm.CT), qd = dq_qt(pl.dm.DP, dq_cw(p, pl.dm));
-  if (w.fwd) consider(p.M, p.N, qf, p.C);
-  if (w.dq) consider(p.M, p.N, qd, p.D);
+  if (w.fwd && !w.fused()) consider(p.M, p.N, qf, p.C);
+  if (w.dq) {
+    const int sp = consider(p.M, p.N, qd, p.D);
+    if (w.fused() && sp > 1) part_s = (size_t)sp * p.M * p.C * 4;
+  }
   if (w.dk) consider(p.N, p.M, qd, p.D);
   if (w.dv) consider(p.N, p.M, qf, p.C);
-  pl.part_bytes = part;
   pl.part = part ? cv.take<float>(part) : nullptr;
+  pl.part_s = part_s ? cv.take<float>(part_s) : nullptr;
   pl.total = cv.off;
 }
 
@@ -399,22 +411,33 @@ void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t 
 // dq-type pass: out[m, :] = tau sum_n Phi(x_m, y_n) <gx_m, vy_n> (y_n - x_m).
 // g1 / g1_dt: the caller's single-channel upstream gradient of the query rows
 // (C = 1), read exactly in the epilogue.
+// With out_s != NULL the forward sum over the same pairs is produced by the
+// same kernel (values vks: V^T in KS layout, unused for C = 1).
 void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const float* scal,
              const uint32_t* kslot, const uint16_t* vrt, const uint32_t* vslot, const uint16_t* grt,
-             const uint32_t* gslot, const void* g1, gs_dtype g1_dt, float* out) {
+             const uint32_t* gslot, const void* g1, gs_dtype g1_dt, float* out,
+             const uint16_t* vks = nullptr, float* out_s = nullptr) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
   const int cw = dq_cw(p, dm);
+  const bool fused = out_s != nullptr;
   PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, cw));
-  DqFn fn = p.qk_dtype == GS_F16 ? dq_fn<F16>(dm.DP, cw) : dq_fn<BF16>(dm.DP, cw);
-  float* dst = ps.splits > 1 ? c.pl->part : out;
+  DqFn fn = p.qk_dtype == GS_F16 ? dq_fn<F16>(dm.DP, cw, dm.CT, fused)
+                                 : dq_fn<BF16>(dm.DP, cw, dm.CT, fused);
+  const bool split = ps.splits > 1;
+  float* dst = split ? c.pl->part : out;
+  float* dst_s = fused ? (split ? c.pl->part_s : out_s) : nullptr;
   prof_before(kKindGrad, c.st);
   fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
      ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)ks.ks,
      p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot, (const uint4*)grt, gslot, g1,
-     (int)g1_dt, c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst, ps.splits > 1 ? nq * p.D : 0);
+     (int)g1_dt, c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst, split ? nq * p.D : 0,
+     (const uint4*)vks, (int)p.C, dst_s, split ? nq * p.C : 0);
   prof_after(kKindGrad, c.st);
   combine(c, ps, nq * p.D, out);
+  if (fused && split)
+    hipLaunchKernelGGL(k_combine, dim3(grid1(nq * p.C)), dim3(256), 0, c.st,
+                       (const float*)c.pl->part_s, ps.splits, nq * p.C, out_s);
 }
 
 void fill_zero(hipStream_t st, float* p, int64_t n) {
@@ -524,70 +547,134 @@ int gauss_sum_profile_stop(float* ms, int max) {
   return rc;
 }
 
-size_t gauss_sum_fwd_workspace_size(const gs_problem* p) {
-  if (check_problem(p) != GS_SUCCESS) return 0;
-  if (p->M == 0 || p->N == 0) return 0;
-  Want w;
-  w.fwd = true;
-  Plan pl;
-  make_plan(*p, w, false, nullptr, pl);
-  return pl.total;
-}
+}  // extern "C"
 
-size_t gauss_sum_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv) {
+namespace gs {
+namespace {
+
+size_t workspace_for(const gs_problem* p, bool fwd, int want_dq, int want_dk, int want_dv) {
   if (check_problem(p) != GS_SUCCESS) return 0;
   if (p->M == 0 || p->N == 0) return 0;
   Want w;
+  w.fwd = fwd;
   w.dq = want_dq != 0;
   w.dk = want_dk != 0;
   w.dv = want_dv != 0;
-  if (!w.dq && !w.dk && !w.dv) return 0;
+  if (!w.fwd && !w.dq && !w.dk && !w.dv) return 0;
   Plan pl;
   make_plan(*p, w, false, nullptr, pl);
+  // the plan with q and k aliased never needs more than the separate one
   return pl.total;
+}
+
+// Common body of the three compute entry points: validates everything, then
+// enqueues the prep kernels and the passes for the requested outputs (out:
+// forward sum, dq / dk / dv: gradients; NULL = not requested).
+gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
+              const void* dout, gs_dtype dout_dtype, float* out, float* dq, float* dk, float* dv,
+              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  gs_status st = check_problem(p);
+  if (st != GS_SUCCESS) return st;
+  if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+  const bool grads = dq || dk || dv;
+  if (grads && !valid_dtype(dout_dtype)) return GS_ERR_UNSUPPORTED;
+  const int64_t M = p->M, N = p->N, D = p->D, C = p->C;
+  if (!out && !grads) return M == 0 && N == 0 ? GS_SUCCESS : GS_ERR_NULL_POINTER;
+  if ((M > 0 && (!q || (grads && !dout))) || (N > 0 && (!k || !v))) return GS_ERR_NULL_POINTER;
+  const size_t vs = dsize(p->v_dtype), gsz = dsize(dout_dtype);
+  if ((M > 0 && (!aligned(q, 2) || (grads && !aligned(dout, gsz)))) ||
+      (N > 0 && (!aligned(k, 2) || !aligned(v, vs))) || (out && !aligned(out, 4)) ||
+      (dq && !aligned(dq, 4)) || (dk && !aligned(dk, 4)) || (dv && !aligned(dv, 4)))
+    return GS_ERR_MISALIGNED;
+  Range in[4] = {range_of(q, M * D * 2), range_of(k, N * D * 2), range_of(v, N * C * (int64_t)vs),
+                 range_of(grads ? dout : nullptr, grads ? M * C * (int64_t)gsz : 0)};
+  Range outs[4] = {range_of(out, out ? M * C * 4 : 0), range_of(dq, dq ? M * D * 4 : 0),
+                   range_of(dk, dk ? N * D * 4 : 0), range_of(dv, dv ? N * C * 4 : 0)};
+  for (int a = 0; a < 4; ++a) {
+    for (int b = 0; b < 4; ++b)
+      if (overlap(outs[a], in[b])) return GS_ERR_ALIAS;
+    for (int b = a + 1; b < 4; ++b)
+      if (overlap(outs[a], outs[b])) return GS_ERR_ALIAS;
+  }
+  if (M == 0 || N == 0) {
+    // Empty sums: every requested output is zero.
+    if (M > 0) {
+      fill_zero(stream, out, M * C);
+      fill_zero(stream, dq, M * D);
+    }
+    if (N > 0) {
+      fill_zero(stream, dk, N * D);
+      fill_zero(stream, dv, N * C);
+    }
+    return launch_status();
+  }
+  const bool alias = (q == k) && (M == N);
+  Want w;
+  w.fwd = out != nullptr;
+  w.dq = dq != nullptr;
+  w.dk = dk != nullptr;
+  w.dv = dv != nullptr;
+  Plan pl;
+  make_plan(*p, w, alias, nullptr, pl);
+  if ((st = check_workspace(workspace, workspace_bytes, pl.total)) != GS_SUCCESS) return st;
+  Range rw = range_of(workspace, (int64_t)pl.total);
+  for (int a = 0; a < 4; ++a)
+    if (overlap(outs[a], rw) || overlap(in[a], rw)) return GS_ERR_ALIAS;
+  make_plan(*p, w, alias, workspace, pl);
+
+  Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
+  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
+  const bool one = C == 1;
+  if (alias) {
+    // q.ks serves dk (keys q, signs of dout) unless only dq wants a KS copy
+    const bool q_for_dk = w.dk;
+    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one ? (q_for_dk ? dout : v) : nullptr,
+                q_for_dk ? dout_dtype : p->v_dtype);
+    if (pl.k.ks != pl.q.ks) prep_points_ks(c, k, N, pl.Np, pl.k.ks, pl.slots + 2, v, p->v_dtype);
+  } else {
+    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one && grads ? dout : nullptr, dout_dtype);
+    prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, one ? v : nullptr, p->v_dtype);
+  }
+  if (w.fwd || w.dq || w.dk) prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
+  if (grads) prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
+  if (pl.scal_kv) prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
+  if (pl.scal_qg) prep_scalars(c, pl.q, dout, dout_dtype, M, pl.Mp, pl.slots + 1, pl.scal_qg);
+  const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
+  if (w.fwd && !w.fused()) pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out);
+  if (w.dq)
+    pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1,
+            dout, dout_dtype, dq, pl.v.ks, w.fused() ? out : nullptr);
+  if (w.dk)
+    pass_dq(c, pl.k, N, pl.q, M, pl.scal_qg, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt,
+            pl.slots + 0, v, p->v_dtype, dk);
+  if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv);
+  return launch_status();
+}
+
+}  // namespace
+}  // namespace gs
+
+extern "C" {
+
+size_t gauss_sum_fwd_workspace_size(const gs_problem* p) { return workspace_for(p, true, 0, 0, 0); }
+
+size_t gauss_sum_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv) {
+  if (!want_dq && !want_dk && !want_dv) return 0;
+  return workspace_for(p, false, want_dq, want_dk, want_dv);
+}
+
+size_t gauss_sum_fwd_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv) {
+  return workspace_for(p, true, want_dq, want_dk, want_dv);
 }
 
 gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
                         float* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
-    gs_status st = check_problem(p);
-    if (st != GS_SUCCESS) return st;
-    if ((st = check_tau(tau)) != GS_SUCCESS) return st;
-    const int64_t M = p->M, N = p->N, D = p->D, C = p->C;
-    if (M == 0) return GS_SUCCESS;
-    if (!out || !q || (N > 0 && (!k || !v))) return GS_ERR_NULL_POINTER;
-    if (!aligned(q, 2) || (N > 0 && (!aligned(k, 2) || !aligned(v, dsize(p->v_dtype)))) ||
-        !aligned(out, 4))
-      return GS_ERR_MISALIGNED;
-    Range ro = range_of(out, M * C * 4);
-    if (overlap(ro, range_of(q, M * D * 2)) ||
-        (N > 0 && (overlap(ro, range_of(k, N * D * 2)) ||
-                   overlap(ro, range_of(v, N * C * (int64_t)dsize(p->v_dtype))))))
-      return GS_ERR_ALIAS;
-    if (N == 0) {
-      fill_zero(stream, out, M * C);
-      return launch_status();
-    }
-    const bool alias = (q == k) && (M == N);
-    Want w;
-    w.fwd = true;
-    Plan pl;
-    make_plan(*p, w, alias, nullptr, pl);
-    if ((st = check_workspace(workspace, workspace_bytes, pl.total)) != GS_SUCCESS) return st;
-    Range rw = range_of(workspace, (int64_t)pl.total);
-    if (overlap(ro, rw) || overlap(rw, range_of(q, M * D * 2)) || overlap(rw, range_of(k, N * D * 2)) ||
-        overlap(rw, range_of(v, N * C * (int64_t)dsize(p->v_dtype))))
-      return GS_ERR_ALIAS;
-    make_plan(*p, w, alias, workspace, pl);
-
-    Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
-    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
-    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2);
-    if (!alias) prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3);
-    prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
-    prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
-    pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out);
-    return launch_status();
+    if (p && check_problem(p) == GS_SUCCESS && check_tau(tau) == GS_SUCCESS && p->M == 0)
+      return GS_SUCCESS;
+    if (!out && p) return GS_ERR_NULL_POINTER;
+    return run(p, q, k, v, tau, nullptr, GS_F32, out, nullptr, nullptr, nullptr, workspace,
+               workspace_bytes, stream);
   } catch (...) {
     return GS_ERR_INTERNAL;
   }
@@ -597,79 +684,32 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
                         const void* dout, gs_dtype dout_dtype, float* dq, float* dk, float* dv,
                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
-    gs_status st = check_problem(p);
-    if (st != GS_SUCCESS) return st;
-    if ((st = check_tau(tau)) != GS_SUCCESS) return st;
-    if (!valid_dtype(dout_dtype)) return GS_ERR_UNSUPPORTED;
-    if (!dq && !dk && !dv) return GS_ERR_NULL_POINTER;
-    const int64_t M = p->M, N = p->N, D = p->D, C = p->C;
-    if ((M > 0 && (!q || !dout)) || (N > 0 && (!k || !v))) return GS_ERR_NULL_POINTER;
-    const size_t vs = dsize(p->v_dtype), gsz = dsize(dout_dtype);
-    if ((M > 0 && (!aligned(q, 2) || !aligned(dout, gsz))) ||
-        (N > 0 && (!aligned(k, 2) || !aligned(v, vs))) || (dq && !aligned(dq, 4)) ||
-        (dk && !aligned(dk, 4)) || (dv && !aligned(dv, 4)))
-      return GS_ERR_MISALIGNED;
-    Range in[4] = {range_of(q, M * D * 2), range_of(k, N * D * 2), range_of(v, N * C * (int64_t)vs),
-                   range_of(dout, M * C * (int64_t)gsz)};
-    Range outs[3] = {range_of(dq, dq ? M * D * 4 : 0), range_of(dk, dk ? N * D * 4 : 0),
-                     range_of(dv, dv ? N * C * 4 : 0)};
-    for (int a = 0; a < 3; ++a) {
-      for (int b = 0; b < 4; ++b)
-        if (overlap(outs[a], in[b])) return GS_ERR_ALIAS;
-      for (int b = a + 1; b < 3; ++b)
-        if (overlap(outs[a], outs[b])) return GS_ERR_ALIAS;
+    if (!dq && !dk && !dv) {
+      gs_status st = check_problem(p);
+      if (st != GS_SUCCESS) return st;
+      if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+      return GS_ERR_NULL_POINTER;
     }
-    if (M == 0 || N == 0) {
-      // Empty sums: every requested gradient is zero.
-      if (M > 0) fill_zero(stream, dq, M * D);
-      if (N > 0) {
-        fill_zero(stream, dk, N * D);
-        fill_zero(stream, dv, N * C);
-      }
-      return launch_status();
-    }
-    const bool alias = (q == k) && (M == N);
-    Want w;
-    w.dq = dq != nullptr;
-    w.dk = dk != nullptr;
-    w.dv = dv != nullptr;
-    Plan pl;
-    make_plan(*p, w, alias, nullptr, pl);
-    if ((st = check_workspace(workspace, workspace_bytes, pl.total)) != GS_SUCCESS) return st;
-    Range rw = range_of(workspace, (int64_t)pl.total);
-    for (int a = 0; a < 3; ++a)
-      if (overlap(outs[a], rw)) return GS_ERR_ALIAS;
-    for (int b = 0; b < 4; ++b)
-      if (overlap(in[b], rw)) return GS_ERR_ALIAS;
-    make_plan(*p, w, alias, workspace, pl);
+    return run(p, q, k, v, tau, dout, dout_dtype, nullptr, dq, dk, dv, workspace, workspace_bytes,
+               stream);
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
 
-    Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
-    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
-    const bool one = C == 1;
-    if (alias) {
-      // q.ks serves dk (keys q, signs of dout) unless only dq wants a KS copy
-      const bool q_for_dk = w.dk;
-      prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one ? (q_for_dk ? dout : v) : nullptr,
-                  q_for_dk ? dout_dtype : p->v_dtype);
-      if (pl.k.ks != pl.q.ks)
-        prep_points_ks(c, k, N, pl.Np, pl.k.ks, pl.slots + 2, v, p->v_dtype);
-    } else {
-      prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one ? dout : nullptr, dout_dtype);
-      prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, one ? v : nullptr, p->v_dtype);
+gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, const void* v,
+                            float tau, const void* dout, gs_dtype dout_dtype, float* out, float* dq,
+                            float* dk, float* dv, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+  try {
+    if (!out) {
+      gs_status st = check_problem(p);
+      if (st != GS_SUCCESS) return st;
+      if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+      return GS_ERR_NULL_POINTER;
     }
-    if (w.dq || w.dk) prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
-    prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
-    if (pl.scal_kv) prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
-    if (pl.scal_qg) prep_scalars(c, pl.q, dout, dout_dtype, M, pl.Mp, pl.slots + 1, pl.scal_qg);
-    const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
-    if (w.dq)
-      pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1,
-              dout, dout_dtype, dq);
-    if (w.dk)
-      pass_dq(c, pl.k, N, pl.q, M, pl.scal_qg, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt,
-              pl.slots + 0, v, p->v_dtype, dk);
-    if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv);
-    return launch_status();
+    return run(p, q, k, v, tau, dout, dout_dtype, out, dq, dk, dv, workspace, workspace_bytes,
+               stream);
   } catch (...) {
     return GS_ERR_INTERNAL;
   }

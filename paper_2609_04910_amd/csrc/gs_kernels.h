@@ -76,7 +76,8 @@ __device__ __forceinline__ void dma_x1(__amdgpu_buffer_rsrc_t rs, uint32_t soff,
 // s_waitcnt vmcnt(N), as assembly so that it is kept exactly as written.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
+  static_assert(N >= 0, "vmcnt range");
+  if constexpr (N >= 64) return;  // only in the unused branch of the two-stage ring
   asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
 }
 
@@ -85,29 +86,42 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return (uint32_t)(uintptr_t)(const lds_void*)p;
 }
 
-// Three-stage LDS ring over the key steps [s_begin, s_end): step s+2 streams
-// in while step s is computed, with one barrier per step.  issue(s, k)
-// enqueues the NL loads of step s into stage k; compute(k) consumes stage k.
-template <int NL, typename Issue, typename Compute>
+// LDS ring of NS (3 or 2) stages over the key steps [s_begin, s_end): step
+// s+NS-1 streams in while step s is computed, with one barrier per step.
+// issue(s, k) enqueues the NL loads of step s into stage k; compute(k)
+// consumes stage k.  With three stages the wait for step s leaves the NL
+// loads of step s+1 in flight.
+template <int NS, int NL, typename Issue, typename Compute>
 __device__ __forceinline__ void key_stream(int s_begin, int s_end, Issue issue, Compute compute) {
-  if (s_begin < s_end) issue(s_begin, 0);
-  if (s_begin + 1 < s_end) issue(s_begin + 1, 1);
+  static_assert(NS == 2 || NS == 3, "two or three stages");
+  for (int k = 0; k < NS - 1; ++k)
+    if (s_begin + k < s_end) issue(s_begin + k, k);
   int cur = 0;
   for (int s = s_begin; s < s_end; ++s) {
-    if (s + 1 < s_end)
-      wait_vmcnt<NL>();  // only step s+1 may still be in flight
-    else
+    if constexpr (NS == 3) {
+      if (s + 1 < s_end)
+        wait_vmcnt<NL>();  // only step s+1 may still be in flight
+      else
+        wait_vmcnt<0>();
+    } else {
       wait_vmcnt<0>();
+    }
     // After the barrier step s is visible to all waves and the stage read in
     // step s-1 is free; the empty assembly keeps the compiler from moving
     // memory accesses across it.
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (s + 2 < s_end) issue(s + 2, cur == 0 ? 2 : cur - 1);
+    if (s + NS - 1 < s_end) issue(s + NS - 1, cur == 0 ? NS - 1 : cur - 1);
     compute(cur);
-    cur = cur == 2 ? 0 : cur + 1;
+    cur = cur == NS - 1 ? 0 : cur + 1;
   }
+}
+
+// Stages for a step of `stage_bytes`: three when they fit in 160 KiB of LDS
+// and the per-step load count fits the vmcnt field, else two.
+constexpr int ring_stages(int stage_bytes, int loads) {
+  return (3 * stage_bytes <= 160 * 1024 && loads < 64) ? 3 : 2;
 }
 
 __device__ __forceinline__ float max4(floatx4 a) {
@@ -224,7 +238,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
   constexpr int KCH = 2 * DP;   // 1-KiB chunks of keys per step
   constexpr int NCH = KCH + CT; // + chunks of V^T
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
-  __shared__ __attribute__((aligned(1024))) char lds[3 * STAGE];
+  constexpr int NS = ring_stages(STAGE, NCH + 1);
+  __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -300,7 +315,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
       for (int ct = 0; ct < CT; ++ct) O[qt][ct] = mfma_f16(vr[ct], b, O[qt][ct]);
     }
   };
-  key_stream<NCH + 1>(s_begin, s_end, issue, compute);
+  key_stream<NS, NCH + 1>(s_begin, s_end, issue, compute);
 
   const int ev = scale_exponent(*vslot) - (ONE ? 1 : 0);
 #pragma unroll
@@ -327,7 +342,15 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 // g_m (exact, from the caller's array) multiplies the epilogue.  Row sums
 // sum_n P use v_dot2_f32_f16 on the same fp16 values the dQ MFMA consumes.
 
-template <typename T, int DP, int CW, int QT>
+//
+// FCT > 0 fuses the forward sum into the same pass (the Sec. 3 observation
+// that the query gradient is one more kernel sum over the same pairs): with
+// C = 1 the forward output is the row sum sum_n Phi v_n the gradient already
+// forms; with C > 1 the kernel values Phi (before the multiplication by w) go
+// through one more MFMA against the FCT 16-row tiles of V^T streamed with
+// the keys.  The forward result goes to out_s (M x C, split partials at
+// part_stride_s), exactly as k_fwd would produce it.
+template <typename T, int DP, int CW, int QT, int FCT>
 __global__ __launch_bounds__(kBlockThreads) void k_dq(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
@@ -335,15 +358,18 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
     const uint32_t* __restrict__ vslot, const uint4* __restrict__ gs,
     const uint32_t* __restrict__ gslot, const void* __restrict__ g1, int g1_dtype, float tau2,
     float tau, int64_t M, int D, int steps_total, int steps_per_split, float* __restrict__ out,
-    int64_t part_stride) {
+    int64_t part_stride, const uint4* __restrict__ vt, int C, float* __restrict__ out_s,
+    int64_t part_stride_s) {
   constexpr int DT = 2 * DP;                // 16-row tiles of K^T (KS layout)
   constexpr int KCH = 2 * DP;               // chunks of K (RT) per step
   constexpr int VCH = 2 * CW;               // chunks of V (RT) per step
   constexpr int TCH = DT;                   // chunks of K^T (KS) per step: 32 DP rows x 64 B
-  constexpr int NCH = KCH + VCH + TCH;
+  constexpr int FCH = CW > 0 ? FCT : 0;     // chunks of V^T (KS) per step, fused forward
+  constexpr int NCH = KCH + VCH + TCH + FCH;
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
+  constexpr int NS = ring_stages(STAGE, NCH + 1);
   constexpr int GW = CW > 0 ? CW : 1;       // RT chunks of the upstream gradient
-  __shared__ __attribute__((aligned(1024))) char lds[3 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -352,6 +378,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
   const int s_begin = blockIdx.y * steps_per_split;
   const int s_end = min(steps_total, s_begin + steps_per_split);
   out += blockIdx.y * part_stride;
+  if constexpr (FCT > 0) out_s += blockIdx.y * part_stride_s;
 
   const bool mine = g == wave;
   // buffer resources over this split's part of each key-side stream
@@ -362,6 +389,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
                             nsteps * VCH * 1024);
   const auto rt = make_rsrc(reinterpret_cast<const char*>(kt_ks) + (int64_t)s_begin * TCH * 1024,
                             nsteps * TCH * 1024);
+  const auto rf = make_rsrc(reinterpret_cast<const char*>(vt) + (int64_t)s_begin * FCH * 1024,
+                            nsteps * FCH * 1024);
   const auto rsc = make_rsrc(scal + (int64_t)s_begin * kScalarFloats, nsteps * kScalarFloats * 4);
   const uint32_t lds0 = lds_address(lds);
   auto issue = [&](int s, int stage) {
@@ -375,6 +404,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
 #pragma unroll
     for (int c = 0; c < TCH; ++c)
       dma_x4(rt, (ls * TCH + c) * 1024, base + (KCH + VCH + c) * 1024, 16 * lane);
+#pragma unroll
+    for (int c = 0; c < FCH; ++c)
+      dma_x4(rf, (ls * FCH + c) * 1024, base + (KCH + VCH + TCH + c) * 1024, 16 * lane);
     dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
   };
 
@@ -393,11 +425,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
 
   floatx4 dQ[QT][DT];
   float rs[QT];
+  floatx4 O[QT][FCH > 0 ? FCH : 1];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     rs[qt] = 0.0f;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) dQ[qt][dt] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ct = 0; ct < FCH; ++ct) O[qt][ct] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
   }
 
   auto compute = [&](int stage) {
@@ -421,9 +456,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
     uint4 ktr[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + j) * 4 + g];
+    uint4 vtr[FCH > 0 ? FCH : 1];
+    const uint4* fb = reinterpret_cast<const uint4*>(base + (KCH + VCH + TCH) * 1024);
+#pragma unroll
+    for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + j) * 4 + g];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-      float p[2][4];
+      float p[2][4], phi[2][4];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         const floatx4 acc = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
@@ -432,11 +471,19 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
 #pragma unroll
           for (int cw = 0; cw < CW; ++cw) w = mfma_f16(vr[kt][cw], greg[qt][cw], w);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[r], tau2, bq[qt])) * w[r];
+          for (int r = 0; r < 4; ++r) {
+            phi[kt][r] = exp2_clamped(fmaf(acc[r], tau2, bq[qt]));
+            p[kt][r] = phi[kt][r] * w[r];
+          }
         } else {
 #pragma unroll
           for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[r], tau2, bq[qt]));
         }
+      }
+      if constexpr (FCH > 0) {
+        const uint4 bphi = pack_tile_pair(phi);
+#pragma unroll
+        for (int ct = 0; ct < FCH; ++ct) O[qt][ct] = mfma_f16(vtr[ct], bphi, O[qt][ct]);
       }
       const uint4 b = pack_tile_pair(p);
 #pragma unroll
@@ -444,7 +491,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
       rs[qt] = dot2_acc(b, sg, rs[qt]);
     }
   };
-  key_stream<NCH + 1>(s_begin, s_end, issue, compute);
+  key_stream<NS, NCH + 1>(s_begin, s_end, issue, compute);
 
   const int ek = kslot ? scale_exponent(*kslot) : 0;
   const uint16_t* q16 = reinterpret_cast<const uint16_t*>(qs);
@@ -453,6 +500,28 @@ __global__ __launch_bounds__(kBlockThreads) void k_dq(
   for (int qt = 0; qt < QT; ++qt) {
     rs[qt] += __shfl_xor(rs[qt], 16, kWave);
     rs[qt] += __shfl_xor(rs[qt], 32, kWave);
+  }
+  if constexpr (FCT > 0) {
+    // fused forward output: single channel from the signed row sums (values
+    // scaled by 2^(ev-1)), several channels from the extra MFMA (2^ev)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      const int64_t m = q0 + 16 * qt + j;
+      if (m >= M) continue;
+      const float f = exp2f(off[qt]);
+      if constexpr (CW == 0) {
+        if (g == 0) out_s[m] = ldexpf(rs[qt] * f, 1 - scale_exponent(*vslot));
+      } else {
+        const int ev = scale_exponent(*vslot);
+#pragma unroll
+        for (int ct = 0; ct < FCH; ++ct)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int c = 16 * ct + 4 * g + r;
+            if (c < C) out_s[m * C + c] = ldexpf(O[qt][ct][r] * f, -ev);
+          }
+      }
+    }
   }
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {

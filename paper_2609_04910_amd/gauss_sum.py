@@ -8,7 +8,10 @@ missing or a call fails, an exception is raised.
 Entry points mirror the C names:
   gauss_sum_fwd(q, k, v, tau)                       -> s        (Eq. 1)
   gauss_sum_bwd(q, k, v, tau, dout, want=...)       -> dq, dk, dv
-  gauss_sum_fwd_workspace_size / gauss_sum_bwd_workspace_size
+  gauss_sum_fwd_bwd(q, k, v, tau, dout, want=...)   -> s, dq, dk, dv (one call;
+                                                       s and dq from one pass)
+  gauss_sum_fwd_workspace_size / gauss_sum_bwd_workspace_size /
+  gauss_sum_fwd_bwd_workspace_size
   gauss_sum_status_string / gauss_sum_abi_version
 and ``GaussSum`` wraps both in a torch.autograd.Function.
 """
@@ -24,9 +27,10 @@ STATUS = {
     4: "GS_ERR_UNSUPPORTED", 5: "GS_ERR_MISALIGNED", 6: "GS_ERR_WORKSPACE", 7: "GS_ERR_HIP",
     8: "GS_ERR_INTERNAL", 9: "GS_ERR_ALIAS",
 }
-EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_workspace_size",
-            "gauss_sum_bwd_workspace_size", "gauss_sum_status_string", "gauss_sum_abi_version",
-            "gauss_sum_profile_start", "gauss_sum_profile_stop")
+EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_bwd", "gauss_sum_fwd_workspace_size",
+            "gauss_sum_bwd_workspace_size", "gauss_sum_fwd_bwd_workspace_size",
+            "gauss_sum_status_string", "gauss_sum_abi_version", "gauss_sum_profile_start",
+            "gauss_sum_profile_stop")
 PROFILE_FWD, PROFILE_GRAD = 1, 2
 
 
@@ -64,6 +68,11 @@ def load(path=LIB_PATH):
     lib.gauss_sum_bwd.argtypes = [P, vp, vp, vp, ctypes.c_float, vp, ctypes.c_int, f32p, f32p, f32p,
                                   vp, sz, vp]
     lib.gauss_sum_bwd.restype = ctypes.c_int
+    lib.gauss_sum_fwd_bwd.argtypes = [P, vp, vp, vp, ctypes.c_float, vp, ctypes.c_int, f32p, f32p,
+                                      f32p, f32p, vp, sz, vp]
+    lib.gauss_sum_fwd_bwd.restype = ctypes.c_int
+    lib.gauss_sum_fwd_bwd_workspace_size.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    lib.gauss_sum_fwd_bwd_workspace_size.restype = sz
     lib.gauss_sum_status_string.argtypes = [ctypes.c_int]
     lib.gauss_sum_status_string.restype = ctypes.c_char_p
     lib.gauss_sum_abi_version.argtypes = []
@@ -125,6 +134,13 @@ def gauss_sum_bwd_workspace_size(M, N, D, C, qk_dtype=GS_F16, v_dtype=GS_F32, wa
     p = make_problem(M, N, D, C, qk_dtype, v_dtype)
     return int(load().gauss_sum_bwd_workspace_size(ctypes.byref(p), int(bool(want_dq)),
                                                    int(bool(want_dk)), int(bool(want_dv))))
+
+
+def gauss_sum_fwd_bwd_workspace_size(M, N, D, C, qk_dtype=GS_F16, v_dtype=GS_F32, want_dq=True,
+                                     want_dk=True, want_dv=True):
+    p = make_problem(M, N, D, C, qk_dtype, v_dtype)
+    return int(load().gauss_sum_fwd_bwd_workspace_size(ctypes.byref(p), int(bool(want_dq)),
+                                                       int(bool(want_dk)), int(bool(want_dv))))
 
 
 def _ptr(t):
@@ -202,6 +218,38 @@ def gauss_sum_bwd(q, k, v, tau, dout, want=(True, True, True), workspace=None, s
     if st != 0:
         raise GaussSumError(st, "gauss_sum_bwd")
     return dq, dk, dv
+
+
+def gauss_sum_fwd_bwd(q, k, v, tau, dout, want=(True, True, True), out=None, workspace=None,
+                      stream=None):
+    """(s, dq, dk, dv) in one call for a known upstream gradient dout; the
+    forward sum and dq come from one pass over the pairs."""
+    import torch
+    _check_inputs(q, k, v)
+    M, D = q.shape
+    N, C = v.shape
+    if not dout.is_cuda or dout.shape != (M, C) or not dout.is_contiguous():
+        raise ValueError("dout must be a contiguous %d x %d GPU tensor" % (M, C))
+    p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
+    lib = load()
+    dev = q.device
+    if out is None:
+        out = torch.empty((M, C), dtype=torch.float32, device=dev)
+    dq = torch.empty((M, D), dtype=torch.float32, device=dev) if want[0] else None
+    dk = torch.empty((N, D), dtype=torch.float32, device=dev) if want[1] else None
+    dv = torch.empty((N, C), dtype=torch.float32, device=dev) if want[2] else None
+    need = int(lib.gauss_sum_fwd_bwd_workspace_size(ctypes.byref(p), int(bool(want[0])),
+                                                    int(bool(want[1])), int(bool(want[2]))))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, dev)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_fwd_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), float(tau), _ptr(dout),
+                               _dtype_code(dout.dtype), _ptr(out), _ptr(dq), _ptr(dk), _ptr(dv),
+                               _ptr(workspace), wbytes, _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_fwd_bwd")
+    return out, dq, dk, dv
 
 
 def _make_autograd():

@@ -40,19 +40,25 @@ def gpu_inputs(w, alias=True):
     return q, k, v, g
 
 
-def run(w, passes, alias=True, g=None):
-    """Runs the requested passes on the GPU; returns numpy fp32 results."""
+def run(w, passes, alias=True, g=None, fused=False):
+    """Runs the requested passes on the GPU (separate gauss_sum_fwd /
+    gauss_sum_bwd calls, or one gauss_sum_fwd_bwd call when fused); returns
+    numpy fp32 results."""
     import torch
     q, k, v, gd = gpu_inputs(w, alias)
     if g is not None:
         gd = to_torch(g)
     res = {}
-    if "fwd" in passes:
-        res["fwd"] = gs.gauss_sum_fwd(q, k, v, float(w.tau))
     want = tuple(p in passes for p in ("dq", "dk", "dv"))
-    if any(want):
-        dq, dk, dv = gs.gauss_sum_bwd(q, k, v, float(w.tau), gd, want=want)
-        res.update({"dq": dq, "dk": dk, "dv": dv})
+    if fused:
+        s, dq, dk, dv = gs.gauss_sum_fwd_bwd(q, k, v, float(w.tau), gd, want=want)
+        res.update({"fwd": s, "dq": dq, "dk": dk, "dv": dv})
+    else:
+        if "fwd" in passes:
+            res["fwd"] = gs.gauss_sum_fwd(q, k, v, float(w.tau))
+        if any(want):
+            dq, dk, dv = gs.gauss_sum_bwd(q, k, v, float(w.tau), gd, want=want)
+            res.update({"dq": dq, "dk": dk, "dv": dv})
     torch.cuda.synchronize()
     return {k_: t.cpu().numpy() for k_, t in res.items() if t is not None}
 
@@ -86,21 +92,33 @@ def compare(label, got, ref, scale, tol):
     return worst, rel_l2
 
 
-def check_workload(w, passes=None, rows=None, key_rows=None, alias=True, label=None):
+def check_workload(w, passes=None, rows=None, key_rows=None, alias=True, label=None, fused=None):
     """Runs ``passes`` on the GPU and checks them against the oracle (all rows,
-    or the given query rows / key rows).  Returns a dict of (max err/A, rel-L2)."""
+    or the given query rows / key rows).  With passes holding the forward and
+    a gradient, both the separate calls and the fused gauss_sum_fwd_bwd call
+    are checked (fused=None), or only one of them (fused=False / True).
+    Returns a dict of (max err/A, rel-L2)."""
     passes = passes or w.passes
     label = label or w.name
-    if w.g is None and any(p in passes for p in ("dq", "dk", "dv")):
+    grads = any(p in passes for p in ("dq", "dk", "dv"))
+    if w.g is None and grads:
         w.g = np.random.default_rng(99).standard_normal((w.M, w.C)).astype(np.float32)
-    got = run(w, passes, alias=alias)
+    modes = [False, True] if fused is None and grads and "fwd" in passes else [bool(fused)]
+    results = [(f, run(w, passes, alias=alias, fused=f)) for f in modes]
     tol = TOL[w.qk_dtype]
     stats = {}
     for p in passes:
         r = key_rows if p in ("dk", "dv") else rows
         ref, scale = oracle_ref(w, p, rows=r)
-        g = got[p] if r is None else got[p][np.asarray(r)]
-        stats[p] = compare("%s/%s" % (label, p), g, ref, scale, tol)
+        for f, got in results:
+            g = got[p] if r is None else got[p][np.asarray(r)]
+            key = p + ("/fused" if f else "")
+            stats[key] = compare("%s/%s" % (label, key), g, ref, scale, tol)
+    if len(results) == 2:
+        sep, fus = results[0][1], results[1][1]
+        for p in ("dk", "dv"):
+            if p in sep:
+                assert np.array_equal(sep[p], fus[p]), "%s: fused %s differs" % (label, p)
     return stats
 
 

@@ -92,6 +92,23 @@ def test_bwd_validation(kw, status):
     assert _bwd(**kw) == status
 
 
+def _fb(M=8, N=8, D=4, C=2, out=FAKE + 0x30000, dq=FAKE + 0x40000, dk=None, dv=None,
+        dout=FAKE + 0x70000, wsb=1 << 40):
+    lib = gs.load()
+    prob = gs.make_problem(M, N, D, C, gs.GS_F16, gs.GS_F32)
+    return lib.gauss_sum_fwd_bwd(ctypes.byref(prob), FAKE, FAKE + 0x10000, FAKE + 0x20000,
+                                 ctypes.c_float(1.0), dout, gs.GS_F32, out, dq, dk, dv,
+                                 FAKE + 0x100000, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(out=None), 1), (dict(dout=None), 1), (dict(out=FAKE + 0x40000), 9),
+    (dict(out=FAKE + 0x70000), 9), (dict(wsb=8), 6), (dict(D=0), 2),
+])
+def test_fwd_bwd_validation(kw, status):
+    assert _fb(**kw) == status
+
+
 def test_empty_query_set_is_a_noop():
     # M = 0: nothing to compute; no pointer is touched and no kernel runs.
     assert _fwd(M=0, q=None, out=None) == 0
@@ -109,6 +126,11 @@ def test_workspace_sizes():
     full = gs.gauss_sum_bwd_workspace_size(1000, 3000, 64, 4)
     only_dq = gs.gauss_sum_bwd_workspace_size(1000, 3000, 64, 4, want_dk=False, want_dv=False)
     assert 0 < only_dq < full
+    fused = gs.gauss_sum_fwd_bwd_workspace_size(1000, 3000, 64, 4, want_dk=False, want_dv=False)
+    assert fused >= only_dq and fused > 0
+    assert gs.gauss_sum_fwd_bwd_workspace_size(1000, 3000, 64, 4, want_dq=False, want_dk=False,
+                                               want_dv=False) == \
+        gs.gauss_sum_fwd_workspace_size(1000, 3000, 64, 4)
 
 
 def test_profile_hook_arguments():
@@ -127,3 +149,4 @@ def test_no_device_reports_hip_error():
         pytest.skip("a GPU is visible")
     assert _fwd() == 7
     assert _bwd() == 7
+    assert _fb() == 7

@@ -62,6 +62,8 @@ def test_small_shapes_all_outputs(shape):
     w = parity.random_workload(SHAPES.index(shape), M, N, D, C, qk, vd, gd, tau, spread)
     stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
     _say("  max err/A and rel-L2:", stats)
+    # the fused call with only dq requested (forward + dq from one pass)
+    parity.check_workload(w, passes=("fwd", "dq"), fused=True)
 
 
 def test_same_points_alias_matches_separate_arrays():
