@@ -14,15 +14,29 @@ svgd (forward + dq, dk, dv), mixture_d32 (forward, --tau), rect_d256
 (forward + dq, dk, dv).
 
 Protocol: inputs are generated on the host (seeded), copied to HBM before
-timing; W untimed warm-up steps, then exactly K steps bracketed by device
-synchronisation, timed with HIP events on the stream the library runs on.
-The dominant kernel's per-launch duration is measured with the library's
-event hook over the same timed steps.  The fp64 CPU oracle is timed on a
-bounded sample of query rows of the same workload (rank 0, one GPU only).
+timing.  The step is first repeated, untimed, for --settle-ms of wall time:
+under sustained matrix-core load the MI355X takes some tens of milliseconds
+to reach its steady shader clock (short bursts run up to ~15 % slower), and a
+production loop runs at the steady clock.  Then W untimed warm-up steps and
+exactly K steps bracketed by device synchronisation, timed with HIP events on
+the stream the library runs on.  The dominant kernel's per-launch duration is
+measured with the library's event hook over the same timed steps.  The fp64
+CPU oracle is timed on a bounded sample of query rows of the same workload
+(rank 0, one GPU only).
+
+roofline.traffic: HBM bytes per launch of the dominant kernel, from the
+rocprofv3 FETCH_SIZE and WRITE_SIZE counters (one --pmc run each), scaled by
+what the same counters read for a device copy of known size run in the same
+process (--calibrate-copy); recorded by --traffic-from into
+profiles/traffic_<workload>.json together with a hash of the kernel sources,
+and reported only while that hash matches the sources (else null).
 
 Prints one JSON line.
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -63,6 +77,69 @@ def flops_per_pair(passes, D, C, fused):
     return f
 
 
+KERNELS = {"fused": "k_dq", "grad": "k_dq", "fwd": "k_fwd"}
+COPY_KERNEL_HINT = "copy"  # torch's device-to-device copy kernel name contains it
+
+
+def kernel_sources_hash():
+    """sha256 over the HIP sources of the library (the kernels the counters measured)."""
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2609_04910_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+
+
+def read_counter_csv(d, counter):
+    """{kernel name: [value per dispatch]} for `counter` from a rocprofv3 csv output dir."""
+    out = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return out
+
+
+def traffic_from(workload, fetch_dir, write_dir, copy_bytes, dominant):
+    """Record HBM bytes per launch of the dominant kernel from two --pmc runs."""
+    rec = {"workload": workload, "kernel": dominant, "kernel_sources_sha256": kernel_sources_hash()}
+    for key, d, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        vals = read_counter_csv(d, counter)
+        dom = [v for name, vs in vals.items() if dominant in name for v in vs]
+        cpy = [v for name, vs in vals.items() if COPY_KERNEL_HINT in name.lower() for v in vs]
+        if not dom or not cpy:
+            raise SystemExit("traffic: no %s samples for %s / the copy kernel in %s" % (counter, dominant, d))
+        kib_dom = sorted(dom)[len(dom) // 2]          # median over dispatches
+        kib_cpy = max(cpy)                            # the calibration copies are the largest
+        factor = copy_bytes / (kib_cpy * 1024.0)      # bytes moved per counted byte
+        rec[key] = {"counter_kib_per_launch": kib_dom, "copy_counter_kib": kib_cpy,
+                    "copy_bytes_each_way": copy_bytes, "scale": factor,
+                    "bytes_per_launch": kib_dom * 1024.0 * factor}
+    rec["bytes_per_launch"] = rec["fetch"]["bytes_per_launch"] + rec["write"]["bytes_per_launch"]
+    with open(traffic_file(workload), "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec))
+
+
+def recorded_traffic(workload, dominant):
+    """Bytes per launch recorded for these kernel sources, else None."""
+    try:
+        with open(traffic_file(workload)) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel") != dominant or rec.get("kernel_sources_sha256") != kernel_sources_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
 def describe(w, passes):
     return ("%s: M=%d queries, N=%d keys, D=%d, C=%d, %s points, tau=%.6g, passes %s"
             % (w.name, w.M, w.N, w.D, w.C, w.qk_dtype, float(w.tau), "+".join(passes)))
@@ -98,14 +175,20 @@ def cpu_baseline(w, passes, budget_s=15.0):
     run(np.arange(1), np.arange(1))
     nq = min(w.M, max(threads, 16))
     nk = min(w.N, max(1, int(nq * w.M / max(w.N, 1)) or 1))
-    t = run(np.arange(nq), np.arange(nk))
-    scale = max(1.0, budget_s / max(t, 1e-3))
-    nq2 = int(min(w.M, max(nq, nq * scale)))
-    nk2 = int(min(w.N, max(nk, nk * scale)))
     rng = np.random.default_rng(3)
-    rows_q = np.sort(rng.choice(w.M, size=nq2, replace=False))
-    rows_k = np.sort(rng.choice(w.N, size=nk2, replace=False))
-    t = run(rows_q, rows_k)
+    t = run(np.arange(nq), np.arange(nk))
+    # grow the sample until it takes at least half the budget (the first
+    # calls include thread start-up, so one extrapolation can undershoot)
+    for _ in range(4):
+        if t >= 0.5 * budget_s or (nq >= w.M and nk >= w.N):
+            break
+        scale = min(64.0, max(1.5, budget_s / max(t, 1e-3)))
+        nq = int(min(w.M, max(nq + 1, nq * scale)))
+        nk = int(min(w.N, max(nk + 1, nk * scale)))
+        rows_q = np.sort(rng.choice(w.M, size=nq, replace=False))
+        rows_k = np.sort(rng.choice(w.N, size=nk, replace=False))
+        t = run(rows_q, rows_k)
+    nq2, nk2 = nq, nk
     # every pass over the sample costs (sampled rows x all partners) pairs; the
     # metric counts a pair once per step, so the rate is sample pairs / time
     has_q = any(p in ("fwd", "dq") for p in passes)
@@ -127,8 +210,14 @@ def cpu_baseline(w, passes, budget_s=15.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=8)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--settle-ms", type=float, default=400.0,
+                    help="untimed repetition of the step before the warm-up, for the steady clock")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="also run a device copy of MIB MiB (counter calibration for --traffic-from)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="record roofline traffic from two rocprofv3 --pmc csv outputs and exit")
     ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES))
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -137,6 +226,11 @@ def main():
                     help="time separate gauss_sum_fwd + gauss_sum_bwd calls instead of one "
                          "gauss_sum_fwd_bwd call")
     args = ap.parse_args()
+    if args.traffic_from:
+        grads_taken = any(p != "fwd" for p in PASSES[args.workload])
+        traffic_from(args.workload, args.traffic_from[0], args.traffic_from[1],
+                     args.calibrate_copy * 1024 * 1024, "k_dq" if grads_taken else "k_fwd")
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -193,6 +287,22 @@ def main():
         if any(grads):
             gs.gauss_sum_bwd(q, k, v, float(w.tau), g, want=grads, workspace=ws, stream=stream)
 
+    if args.calibrate_copy:
+        nb = args.calibrate_copy * 1024 * 1024
+        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    settle_steps = 0
+    t_settle = time.perf_counter()
+    while settle_steps == 0 or (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        step()
+        settle_steps += 1
+        torch.cuda.synchronize()
+    settle_ms = (time.perf_counter() - t_settle) * 1e3
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -239,6 +349,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": {"ms": settle_ms, "steps": settle_steps},
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -258,7 +369,7 @@ def main():
             "peak": PEAK_MFMA_F16 / 1e12,
             "unit": "TFLOP/s",
             "frac": achieved / (PEAK_MFMA_F16 / 1e12),
-            "traffic": None,
+            "traffic": recorded_traffic(args.workload, "k_dq" if any(grads) else "k_fwd"),
             "avg_launch_ms": avg_kernel_ms,
             "launches": len(kernel_ms),
             "flops_per_launch": dom_flops,

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "gs_common.h"
@@ -19,8 +20,9 @@ namespace gs {
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kTargetBlocks = 1024;   // workgroups per pass before splitting over keys
-constexpr int kMinStepsPerSplit = 4;  // 128 keys
+constexpr int kMinStepsPerSplit = 4;     // 128 keys
+constexpr int kSplitOverheadSteps = 8;   // per-workgroup fixed cost (prologue, epilogue), in key steps
+constexpr int kDefaultSlots = 512;       // resident workgroups assumed when no device can be queried
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
@@ -74,29 +76,41 @@ void launch_fwd(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, co
                      nhq, srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride);
 }
 
+// A launcher and the kernel it launches (for occupancy queries).
+struct FwdK {
+  FwdFn launch = nullptr;
+  const void* kernel = nullptr;
+};
+
+template <typename T, int DP, int CT, bool ONE>
+FwdK fwd_k() {
+  return {&launch_fwd<T, DP, CT, ONE>,
+          reinterpret_cast<const void*>(&k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE>)};
+}
+
 // CT = 0 selects the single-channel form (one 16-row tile of signs).
 template <typename T, int DP>
-FwdFn fwd_by_ct(int CT) {
+FwdK fwd_by_ct(int CT) {
   switch (CT) {
-    case 0: return &launch_fwd<T, DP, 1, true>;
-    case 1: return &launch_fwd<T, DP, 1, false>;
-    case 2: return &launch_fwd<T, DP, 2, false>;
-    case 4: return &launch_fwd<T, DP, 4, false>;
-    case 8: return &launch_fwd<T, DP, 8, false>;
-    case 16: return &launch_fwd<T, DP, 16, false>;
+    case 0: return fwd_k<T, DP, 1, true>();
+    case 1: return fwd_k<T, DP, 1, false>();
+    case 2: return fwd_k<T, DP, 2, false>();
+    case 4: return fwd_k<T, DP, 4, false>();
+    case 8: return fwd_k<T, DP, 8, false>();
+    case 16: return fwd_k<T, DP, 16, false>();
   }
-  return nullptr;
+  return {};
 }
 
 template <typename T>
-FwdFn fwd_fn(int DP, int CT) {
+FwdK fwd_fn(int DP, int CT) {
   switch (DP) {
     case 1: return fwd_by_ct<T, 1>(CT);
     case 2: return fwd_by_ct<T, 2>(CT);
     case 4: return fwd_by_ct<T, 4>(CT);
     case 8: return fwd_by_ct<T, 8>(CT);
   }
-  return nullptr;
+  return {};
 }
 
 using DqFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
@@ -116,14 +130,25 @@ void launch_dq(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, con
                      D, steps, sps, out, pstride, vt, C, out_s, pstride_s);
 }
 
+struct DqK {
+  DqFn launch = nullptr;
+  const void* kernel = nullptr;
+};
+
+template <typename T, int DP, int CW, int FCT>
+DqK dq_k() {
+  return {&launch_dq<T, DP, CW, FCT>,
+          reinterpret_cast<const void*>(&k_dq<T, DP, CW, dq_qt(DP, CW), FCT>)};
+}
+
 // fused: also produce the forward sum (FCT = 1 for C = 1, else the V^T tiles).
 template <typename T, int DP, int CW, int CTF>
-DqFn dq_pick(bool fused) {
-  return fused ? &launch_dq<T, DP, CW, CTF> : &launch_dq<T, DP, CW, 0>;
+DqK dq_pick(bool fused) {
+  return fused ? dq_k<T, DP, CW, CTF>() : dq_k<T, DP, CW, 0>();
 }
 
 template <typename T, int DP>
-DqFn dq_by_cw(int CW, int CT, bool fused) {
+DqK dq_by_cw(int CW, int CT, bool fused) {
   switch (CW) {
     case 0: return dq_pick<T, DP, 0, 1>(fused);
     case 1: return CT == 2 ? dq_pick<T, DP, 1, 2>(fused) : dq_pick<T, DP, 1, 1>(fused);
@@ -131,18 +156,18 @@ DqFn dq_by_cw(int CW, int CT, bool fused) {
     case 4: return dq_pick<T, DP, 4, 8>(fused);
     case 8: return dq_pick<T, DP, 8, 16>(fused);
   }
-  return nullptr;
+  return {};
 }
 
 template <typename T>
-DqFn dq_fn(int DP, int CW, int CT, bool fused) {
+DqK dq_fn(int DP, int CW, int CT, bool fused) {
   switch (DP) {
     case 1: return dq_by_cw<T, 1>(CW, CT, fused);
     case 2: return dq_by_cw<T, 2>(CW, CT, fused);
     case 4: return dq_by_cw<T, 4>(CW, CT, fused);
     case 8: return dq_by_cw<T, 8>(CW, CT, fused);
   }
-  return nullptr;
+  return {};
 }
 
 // ------------------------------------------------------------ workspace plan
@@ -189,13 +214,57 @@ struct PassShape {
   int blocks, splits, sps, steps;
 };
 
-PassShape pass_shape(int64_t rows, int64_t keys, int QT) {
+// Workgroups of `kernel` resident on the current device at once (CUs times
+// workgroups per CU), cached per kernel and device; kDefaultSlots when no
+// device can be queried (workspace sizes asked for on a machine without one).
+int device_slots(const void* kernel) {
+  struct Entry {
+    const void* kernel;
+    int device, slots;
+  };
+  static Entry cache[512];
+  static int used = 0;
+  static std::mutex mu;
+  int dev = 0;
+  if (!kernel || hipGetDevice(&dev) != hipSuccess) return kDefaultSlots;
+  std::lock_guard<std::mutex> lock(mu);
+  for (int i = 0; i < used; ++i)
+    if (cache[i].kernel == kernel && cache[i].device == dev) return cache[i].slots;
+  int cus = 0, occ = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return kDefaultSlots;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, kBlockThreads, 0) != hipSuccess ||
+      occ < 1)
+    return kDefaultSlots;
+  const int slots = cus * occ;
+  if (used < 512) cache[used++] = Entry{kernel, dev, slots};
+  return slots;
+}
+
+// Workgroups along the rows, and the split of the key steps into grid.y
+// parts (partial sums combined afterwards): the split count that minimises
+// (rounds of resident workgroups) x (steps per split + fixed cost), searched
+// from the smallest count that fills the device once up to four times that.
+PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel) {
   PassShape ps;
   ps.blocks = (int)ceil_div(rows, 64 * QT);
   ps.steps = (int)ceil_div(keys, kStep);
-  int want = (int)std::max<int64_t>(1, ceil_div(kTargetBlocks, std::max(1, ps.blocks)));
-  int cap = std::max(1, ps.steps / kMinStepsPerSplit);
-  int splits = std::max(1, std::min(want, cap));
+  const int64_t slots = device_slots(kernel);
+  const int cap = std::max(1, ps.steps / kMinStepsPerSplit);
+  const int lo = (int)std::min<int64_t>(cap, std::max<int64_t>(1, ceil_div(slots, std::max(1, ps.blocks))));
+  const int hi = std::min(cap, 4 * lo);
+  auto cost = [&](int sp) {
+    return ceil_div((int64_t)ps.blocks * sp, slots) * (ceil_div(ps.steps, sp) + kSplitOverheadSteps);
+  };
+  int splits = lo;
+  int64_t best = cost(lo);
+  for (int sp = lo + 1; sp <= hi; ++sp) {
+    const int64_t c = cost(sp);
+    if (c * 50 < best * 49) {  // at least 2 % better
+      best = c;
+      splits = sp;
+    }
+  }
   ps.sps = (int)ceil_div(ps.steps, splits);
   ps.splits = ps.steps ? (int)ceil_div(ps.steps, ps.sps) : 1;
   return ps;
@@ -207,6 +276,17 @@ struct Want {
 };
 
 inline int dq_cw(const gs_problem& p, const Dims& dm) { return p.C == 1 ? 0 : dm.CW; }
+
+FwdK fwd_for(const gs_problem& p, const Dims& dm) {
+  const int ct = p.C == 1 ? 0 : dm.CT;
+  return p.qk_dtype == GS_F16 ? fwd_fn<F16>(dm.DP, ct) : fwd_fn<BF16>(dm.DP, ct);
+}
+DqK dq_for(const gs_problem& p, const Dims& dm, bool fused) {
+  const int cw = dq_cw(p, dm);
+  return p.qk_dtype == GS_F16 ? dq_fn<F16>(dm.DP, cw, dm.CT, fused) : dq_fn<BF16>(dm.DP, cw, dm.CT, fused);
+}
+const void* fwd_kernel(const gs_problem& p, const Dims& dm) { return fwd_for(p, dm).kernel; }
+const void* dq_kernel(const gs_problem& p, const Dims& dm, bool fused) { return dq_for(p, dm, fused).kernel; }
 
 // Lays out every buffer the requested passes need; with ws == nullptr only
 // computes the size.
@@ -243,26 +323,30 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   }
   if (keys_k) pl.scal_kv = cv.take<float>(pl.Np * 2 * 4);
   if (keys_q) pl.scal_qg = cv.take<float>(pl.Mp * 2 * 4);
-  if (w.dq || w.dk) pl.v.rt = cv.take<uint16_t>(pl.Np * Wv * 2);
+  // RT value copies feed the <g, v> contraction of several channels only
+  // (single-channel gradients fold v into the exponent and the signs)
+  const bool wc = (w.dq || w.dk) && p.C > 1;
+  if (wc) pl.v.rt = cv.take<uint16_t>(pl.Np * Wv * 2);
   if (w.fwd && !(w.fused() && p.C == 1)) pl.v.ks = cv.take<uint16_t>(pl.Np * Rv * 2);
-  if (w.dq || w.dk) pl.g.rt = cv.take<uint16_t>(pl.Mp * Wv * 2);
+  if (wc) pl.g.rt = cv.take<uint16_t>(pl.Mp * Wv * 2);
   if (w.dv) pl.g.ks = cv.take<uint16_t>(pl.Mp * Rv * 2);
 
   // Partial-sum buffer for split passes (reused by every pass in turn).
   size_t part = 0, part_s = 0;
-  auto consider = [&](int64_t rows, int64_t keys, int QT, int64_t width) {
-    PassShape ps = pass_shape(rows, keys, QT);
+  auto consider = [&](int64_t rows, int64_t keys, int QT, int64_t width, const void* kernel) {
+    PassShape ps = pass_shape(rows, keys, QT, kernel);
     if (ps.splits > 1) part = std::max(part, (size_t)ps.splits * rows * width * 4);
     return ps.splits;
   };
   const int qf = fwd_qt(pl.dm.DP, pl.dm.CT), qd = dq_qt(pl.dm.DP, dq_cw(p, pl.dm));
-  if (w.fwd && !w.fused()) consider(p.M, p.N, qf, p.C);
+  const void* kf = fwd_kernel(p, pl.dm);
+  if (w.fwd && !w.fused()) consider(p.M, p.N, qf, p.C, kf);
   if (w.dq) {
-    const int sp = consider(p.M, p.N, qd, p.D);
+    const int sp = consider(p.M, p.N, qd, p.D, dq_kernel(p, pl.dm, w.fused()));
     if (w.fused() && sp > 1) part_s = (size_t)sp * p.M * p.C * 4;
   }
-  if (w.dk) consider(p.N, p.M, qd, p.D);
-  if (w.dv) consider(p.N, p.M, qf, p.C);
+  if (w.dk) consider(p.N, p.M, qd, p.D, dq_kernel(p, pl.dm, false));
+  if (w.dv) consider(p.N, p.M, qf, p.C, kf);
   pl.part = part ? cv.take<float>(part) : nullptr;
   pl.part_s = part_s ? cv.take<float>(part_s) : nullptr;
   pl.total = cv.off;
@@ -302,6 +386,8 @@ void prof_release() {
 inline unsigned grid1(int64_t n, int threads = 256) {
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(n, threads), 1 << 20));
 }
+// Reductions: at most 512 workgroups (grid-stride), one atomic each.
+inline unsigned grid_reduce(int64_t n) { return std::min(grid1(n), 512u); }
 
 struct Ctx {
   hipStream_t st;
@@ -317,21 +403,19 @@ void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t n, int64_t n_pad, 
                    uint32_t* slot, const void* sgn, gs_dtype sgn_dt) {
   const gs_problem& p = *c.p;
   const int W = c.pl->dm.W();
-  hipLaunchKernelGGL(k_points_rt, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D, n_pad,
-                     W, s.rt);
-  hipLaunchKernelGGL(k_points_norm<T>, dim3(grid1(n_pad)), dim3(256), 0, c.st, x16, n, (int)p.D, n_pad,
-                     s.nh);
+  hipLaunchKernelGGL(k_points_rt_norm<T>, dim3(grid1(n_pad * (W / 8))), dim3(256), 0, c.st, x16, n,
+                     (int)p.D, n_pad, W, s.rt, s.nh);
   if (s.samp_rt)
     hipLaunchKernelGGL(k_sample<T>, dim3(grid1(64 * W)), dim3(256), 0, c.st, x16, n, (int)p.D, W,
                        s.samp_rt, s.samp_nh);
   if (s.ks) {
     const uint32_t* sl = nullptr;
     if (p.qk_dtype == GS_BF16) {
-      hipLaunchKernelGGL(k_absmax, dim3(grid1(n * p.D, 256)), dim3(256), 0, c.st,
+      hipLaunchKernelGGL(k_absmax, dim3(grid_reduce(n * p.D)), dim3(256), 0, c.st,
                          static_cast<const void*>(x16), n * p.D, 2, slot);
       sl = slot;
     }
-    hipLaunchKernelGGL(k_points_ks<T>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
+    hipLaunchKernelGGL(k_points_ks<T>, dim3(grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
                        n_pad, W, sl, sgn, (int)sgn_dt, s.ks);
   }
 }
@@ -353,10 +437,10 @@ void prep_points_ks(const Ctx& c, const void* x, int64_t n, int64_t n_pad, uint1
   const uint16_t* x16 = static_cast<const uint16_t*>(x);
   const uint32_t* sl = p.qk_dtype == GS_BF16 ? slot : nullptr;
   if (p.qk_dtype == GS_F16)
-    hipLaunchKernelGGL(k_points_ks<F16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
+    hipLaunchKernelGGL(k_points_ks<F16>, dim3(grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
                        n_pad, W, sl, sgn, (int)sgn_dt, ks);
   else
-    hipLaunchKernelGGL(k_points_ks<BF16>, dim3(grid1(n_pad * W)), dim3(256), 0, c.st, x16, n,
+    hipLaunchKernelGGL(k_points_ks<BF16>, dim3(grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n,
                        (int)p.D, n_pad, W, sl, sgn, (int)sgn_dt, ks);
 }
 
@@ -365,7 +449,7 @@ void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t n, int64_t n_
   const gs_problem& p = *c.p;
   const int Wv = c.pl->dm.Wv(), Rv = c.pl->dm.Rv();
   if (n > 0)
-    hipLaunchKernelGGL(k_absmax, dim3(grid1(n * p.C, 256)), dim3(256), 0, c.st, x, n * p.C, (int)dt,
+    hipLaunchKernelGGL(k_absmax, dim3(grid_reduce(n * p.C)), dim3(256), 0, c.st, x, n * p.C, (int)dt,
                        slot);
   if (s.rt)
     hipLaunchKernelGGL(k_values_rt, dim3(grid1(n_pad * Wv)), dim3(256), 0, c.st, x, (int)dt, n,
@@ -396,9 +480,9 @@ void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t 
               const float* scal, const uint16_t* vks, const uint32_t* vslot, float* out) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
-  PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT));
-  const int ct = p.C == 1 ? 0 : dm.CT;
-  FwdFn fn = p.qk_dtype == GS_F16 ? fwd_fn<F16>(dm.DP, ct) : fwd_fn<BF16>(dm.DP, ct);
+  const FwdK fk = fwd_for(p, dm);
+  PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT), fk.kernel);
+  FwdFn fn = fk.launch;
   float* dst = ps.splits > 1 ? c.pl->part : out;
   prof_before(kKindFwd, c.st);
   fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
@@ -419,11 +503,10 @@ void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t n
              const uint16_t* vks = nullptr, float* out_s = nullptr) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
-  const int cw = dq_cw(p, dm);
   const bool fused = out_s != nullptr;
-  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, cw));
-  DqFn fn = p.qk_dtype == GS_F16 ? dq_fn<F16>(dm.DP, cw, dm.CT, fused)
-                                 : dq_fn<BF16>(dm.DP, cw, dm.CT, fused);
+  const DqK dk = dq_for(p, dm, fused);
+  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, dq_cw(p, dm)), dk.kernel);
+  DqFn fn = dk.launch;
   const bool split = ps.splits > 1;
   float* dst = split ? c.pl->part : out;
   float* dst_s = fused ? (split ? c.pl->part_s : out_s) : nullptr;
@@ -636,7 +719,10 @@ gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, 
     prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, one ? v : nullptr, p->v_dtype);
   }
   if (w.fwd || w.dq || w.dk) prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
-  if (grads) prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
+  // dout: its maximum scales the RT / KS copies (several channels, dv) and
+  // enters the key scalars of passes keyed by q (dk, dv); a single-channel dq
+  // reads dout exactly in its epilogue and needs none of it
+  if (grads && (C > 1 || w.dk || w.dv)) prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
   if (pl.scal_kv) prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
   if (pl.scal_qg) prep_scalars(c, pl.q, dout, dout_dtype, M, pl.Mp, pl.slots + 1, pl.scal_qg);
   const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;

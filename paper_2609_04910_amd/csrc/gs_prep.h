@@ -28,9 +28,11 @@ __global__ void k_fill_f32(float* __restrict__ p, int64_t n, float val) {
 
 
 // max |x| over count elements into *slot (float bits; |x| >= 0 so unsigned
-// comparison of the bit patterns orders them; NaN compares largest).
+// comparison of the bit patterns orders them; NaN compares largest).  Reduced
+// within the workgroup first: one atomic per workgroup.
 __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
                          uint32_t* __restrict__ slot) {
+  __shared__ uint32_t wmax[kWavesPerBlock];
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
   uint32_t mb = 0;
@@ -42,60 +44,82 @@ __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
     uint32_t o = (uint32_t)__shfl_xor((int)mb, off, kWave);
     mb = o > mb ? o : mb;
   }
-  if ((threadIdx.x & (kWave - 1)) == 0 && mb != 0) atomicMax(slot, mb);
-}
-
-// Points: xs[RT] = x (padding rows / columns = 0), one thread per element.
-__global__ void k_points_rt(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad, int W,
-                            uint16_t* __restrict__ xs) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * W; t += stride) {
-    int64_t r = t / W;
-    int w = (int)(t - r * W);
-    uint16_t b = (r < n && w < D) ? x[r * D + w] : (uint16_t)0;
-    xs[rt_index(r, w, W)] = b;
+  if ((threadIdx.x & (kWave - 1)) == 0) wmax[threadIdx.x / kWave] = mb;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kWavesPerBlock; ++w) mb = wmax[w] > mb ? wmax[w] : mb;
+    if (mb != 0) atomicMax(slot, mb);
   }
 }
 
-// nh[r] = -||x_r||^2 / 2 summed in fp64 from the exact input values, rounded
-// once to fp32; padding rows get kPadBias so their kernel value is 0.
+// Points, RT copy and half norms in one pass.  Thread (r, c) moves columns
+// 8c .. 8c+7 of row r (one 16-byte store into the RT copy: those eight
+// columns are contiguous there) and sums their squares in fp64; the W/8
+// threads of a row are consecutive lanes, reduced with shuffles, so
+// nh[r] = -||x_r||^2 / 2 is rounded once to fp32.  Padding rows / columns are
+// zero, padding rows get kPadBias.  n_pad * W/8 is a multiple of the wave
+// size, so every lane of a wave runs the same iterations of the grid-stride
+// loop and the shuffles see whole waves.
 template <typename T>
-__global__ void k_points_norm(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad,
-                              float* __restrict__ nh) {
+__global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad,
+                                 int W, uint16_t* __restrict__ xs, float* __restrict__ nh) {
+  const int cpr = W >> 3;  // threads per row (4, 8, 16 or 32)
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n_pad; r += stride) {
-    if (r >= n) { nh[r] = kPadBias; continue; }
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * cpr; t += stride) {
+    const int64_t r = t / cpr;
+    const int c = (int)(t - r * cpr);
+    uint16_t h[8];
     double acc = 0.0;
-    const uint16_t* row = x + r * D;
-    for (int d = 0; d < D; ++d) {
-      double v = (double)T::to_float(row[d]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int w = 8 * c + e;
+      h[e] = (r < n && w < D) ? x[r * D + w] : (uint16_t)0;
+      const double v = (double)T::to_float(h[e]);
       acc += v * v;
     }
-    nh[r] = (float)(-0.5 * acc);
+    for (int off = cpr >> 1; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
+    uint4 pk;
+    pk.x = h[0] | ((uint32_t)h[1] << 16);
+    pk.y = h[2] | ((uint32_t)h[3] << 16);
+    pk.z = h[4] | ((uint32_t)h[5] << 16);
+    pk.w = h[6] | ((uint32_t)h[7] << 16);
+    *reinterpret_cast<uint4*>(xs + rt_index(r, 8 * c, W)) = pk;
+    if (c == 0) nh[r] = r < n ? (float)(-0.5 * acc) : kPadBias;
   }
 }
-
 
 // Points, KS-layout fp16 copy scaled by 2^e (e from *slot when slot != NULL,
 // needed for bf16 inputs whose range exceeds fp16) and, when sgn != NULL,
-// multiplied by the sign of the single-channel value sgn[r] (exact).  One
-// thread per element, keys fastest so that the writes of a wave stay within a
-// few 64-byte lines.
+// multiplied by the sign of the single-channel value sgn[r] (exact).  Thread
+// (32-key block, row w, quarter a) writes the eight key slots 8a .. 8a+7 of
+// row w (one 16-byte store); consecutive threads write consecutive 16 bytes.
 template <typename T>
 __global__ void k_points_ks(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad, int R,
                             const uint32_t* __restrict__ slot, const void* __restrict__ sgn,
                             int sgn_dtype, uint16_t* __restrict__ xt) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float s = slot ? ldexpf(1.0f, scale_exponent(*slot)) : 1.0f;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * R; t += stride) {
-    int64_t blk = t / (32 * (int64_t)R);
-    int rem = (int)(t - blk * 32 * (int64_t)R);
-    int w = rem >> 5;
-    int64_t r = blk * 32 + (rem & 31);
-    float v = (r < n && w < D) ? T::to_float(x[r * D + w]) * s : 0.0f;
-    if (sgn && r < n && load_any(sgn, r, sgn_dtype) < 0.0f) v = -v;
-    _Float16 h = (_Float16)v;
-    xt[ks_index(r, w, R)] = __builtin_bit_cast(uint16_t, h);
+  const int64_t total = (n_pad >> 5) * R * 4;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
+    const int a = (int)(t & 3);
+    const int64_t rest = t >> 2;
+    const int64_t blk = rest / R;
+    const int w = (int)(rest - blk * R);
+    uint16_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int z = 8 * a + e;
+      const int64_t r = blk * 32 + 16 * ((z & 7) >> 2) + 4 * (z >> 3) + (z & 3);
+      float v = (r < n && w < D) ? T::to_float(x[r * D + w]) * s : 0.0f;
+      if (sgn && r < n && load_any(sgn, r, sgn_dtype) < 0.0f) v = -v;
+      h[e] = __builtin_bit_cast(uint16_t, (_Float16)v);
+    }
+    uint4 pk;
+    pk.x = h[0] | ((uint32_t)h[1] << 16);
+    pk.y = h[2] | ((uint32_t)h[3] << 16);
+    pk.z = h[4] | ((uint32_t)h[5] << 16);
+    pk.w = h[6] | ((uint32_t)h[7] << 16);
+    *reinterpret_cast<uint4*>(xt + ((blk * R + w) * 32 + 8 * a)) = pk;
   }
 }
 
@@ -192,14 +216,31 @@ __global__ void k_step_scalars(const float* __restrict__ nh, const void* __restr
   }
 }
 
-// out[m, w] = sum_s part[s, m, w] in split order (deterministic).
+// out[m, w] = sum_s part[s, m, w] in split order (deterministic); four
+// elements per thread where count allows 16-byte accesses.
 __global__ void k_combine(const float* __restrict__ part, int splits, int64_t count,
                           float* __restrict__ out) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  if ((count & 3) == 0) {
+    const int64_t c4 = count >> 2;
+    const float4* p4 = reinterpret_cast<const float4*>(part);
+    for (; i < c4; i += stride) {
+      float4 acc = p4[i];
+      for (int s = 1; s < splits; ++s) {
+        const float4 v = p4[(int64_t)s * c4 + i];
+        acc.x += v.x;
+        acc.y += v.y;
+        acc.z += v.z;
+        acc.w += v.w;
+      }
+      reinterpret_cast<float4*>(out)[i] = acc;
+    }
+    return;
+  }
   for (; i < count; i += stride) {
-    float acc = 0.0f;
-    for (int s = 0; s < splits; ++s) acc += part[(int64_t)s * count + i];
+    float acc = part[i];
+    for (int s = 1; s < splits; ++s) acc += part[(int64_t)s * count + i];
     out[i] = acc;
   }
 }
