@@ -51,14 +51,18 @@ inline Dims dims_of(int64_t D, int64_t C) {
   return d;
 }
 
-// Query tiles per wave: the largest of 4, 2, 1 whose kernel (as compiled for
-// gfx950) keeps the register count at or below 256 per lane (two waves per
-// SIMD); the D = 256 gradient kernel runs one wave per SIMD.
+// Query tiles per wave.  Forward: the largest of 4, 2, 1 whose kernel (as
+// compiled for gfx950) keeps the register count at or below 256 per lane (two
+// waves per SIMD).  Gradient: for D > 64 two tiles even where that needs the
+// occupancy hint on k_dq or (D = 256, whose LDS ring allows one workgroup per
+// CU anyway) one wave per SIMD: a K tile read from LDS then feeds two MFMAs,
+// and a single tile per wave is bound by LDS bandwidth; D = 256 with
+// C > 128 keeps one tile (two would spill inside the key loop).
 constexpr int fwd_qt(int DP, int CT) {
   return CT >= 16 ? 1 : CT == 8 ? 2 : (DP == 8 && CT > 1) ? 2 : 4;
 }
 constexpr int dq_qt(int DP, int CW) {
-  return DP >= 4 ? 1 : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
+  return DP >= 4 ? (DP == 8 && CW == 8 ? 1 : 2) : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
 }
 
 // ------------------------------------------------------------ dispatch tables
@@ -141,20 +145,23 @@ DqK dq_k() {
           reinterpret_cast<const void*>(&k_dq<T, DP, CW, dq_qt(DP, CW), FCT>)};
 }
 
-// fused: also produce the forward sum (FCT = 1 for C = 1, else the V^T tiles).
-template <typename T, int DP, int CW, int CTF>
+// fused: also produce the forward sum (one 16-row tile: C = 1 through the
+// row sums, 1 < C <= kFuseMaxC through one V^T tile); wider values are never
+// fused (see kFuseMaxC), so those instances do not exist.
+template <typename T, int DP, int CW>
 DqK dq_pick(bool fused) {
-  return fused ? dq_k<T, DP, CW, CTF>() : dq_k<T, DP, CW, 0>();
+  return fused ? dq_k<T, DP, CW, 1>() : dq_k<T, DP, CW, 0>();
 }
 
 template <typename T, int DP>
 DqK dq_by_cw(int CW, int CT, bool fused) {
+  if (fused && CT > 1) return {};
   switch (CW) {
-    case 0: return dq_pick<T, DP, 0, 1>(fused);
-    case 1: return CT == 2 ? dq_pick<T, DP, 1, 2>(fused) : dq_pick<T, DP, 1, 1>(fused);
-    case 2: return dq_pick<T, DP, 2, 4>(fused);
-    case 4: return dq_pick<T, DP, 4, 8>(fused);
-    case 8: return dq_pick<T, DP, 8, 16>(fused);
+    case 0: return dq_pick<T, DP, 0>(fused);
+    case 1: return dq_pick<T, DP, 1>(fused);
+    case 2: return fused ? DqK{} : dq_k<T, DP, 2, 0>();
+    case 4: return fused ? DqK{} : dq_k<T, DP, 4, 0>();
+    case 8: return fused ? DqK{} : dq_k<T, DP, 8, 0>();
   }
   return {};
 }
@@ -270,10 +277,26 @@ PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel) {
   return ps;
 }
 
+// Largest value width whose forward sum rides along in the dq pass: beyond
+// one 16-row tile of V^T the extra contraction and its registers cost more
+// than a separate forward pass.
+constexpr int64_t kFuseMaxC = 16;
+
 struct Want {
   bool fwd = false, dq = false, dk = false, dv = false;
-  bool fused() const { return fwd && dq; }  // forward computed inside the dq pass
+  bool fuse = false;                           // set by want_for: C <= kFuseMaxC
+  bool fused() const { return fwd && dq && fuse; }  // forward computed inside the dq pass
 };
+
+Want want_for(const gs_problem& p, bool fwd, bool dq, bool dk, bool dv) {
+  Want w;
+  w.fwd = fwd;
+  w.dq = dq;
+  w.dk = dk;
+  w.dv = dv;
+  w.fuse = p.C <= kFuseMaxC;
+  return w;
+}
 
 inline int dq_cw(const gs_problem& p, const Dims& dm) { return p.C == 1 ? 0 : dm.CW; }
 
@@ -638,11 +661,7 @@ namespace {
 size_t workspace_for(const gs_problem* p, bool fwd, int want_dq, int want_dk, int want_dv) {
   if (check_problem(p) != GS_SUCCESS) return 0;
   if (p->M == 0 || p->N == 0) return 0;
-  Want w;
-  w.fwd = fwd;
-  w.dq = want_dq != 0;
-  w.dk = want_dk != 0;
-  w.dv = want_dv != 0;
+  Want w = want_for(*p, fwd, want_dq != 0, want_dk != 0, want_dv != 0);
   if (!w.fwd && !w.dq && !w.dk && !w.dv) return 0;
   Plan pl;
   make_plan(*p, w, false, nullptr, pl);
@@ -692,11 +711,14 @@ gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, 
     return launch_status();
   }
   const bool alias = (q == k) && (M == N);
-  Want w;
-  w.fwd = out != nullptr;
-  w.dq = dq != nullptr;
-  w.dk = dk != nullptr;
-  w.dv = dv != nullptr;
+  Want w = want_for(*p, out != nullptr, dq != nullptr, dk != nullptr, dv != nullptr);
+  {
+    // every kernel the passes below launch must exist for this shape
+    const Dims dm = dims_of(D, C);
+    if (((w.fwd && !w.fused()) || w.dv) && !fwd_for(*p, dm).launch) return GS_ERR_INTERNAL;
+    if (w.dq && !dq_for(*p, dm, w.fused()).launch) return GS_ERR_INTERNAL;
+    if (w.dk && !dq_for(*p, dm, false).launch) return GS_ERR_INTERNAL;
+  }
   Plan pl;
   make_plan(*p, w, alias, nullptr, pl);
   if ((st = check_workspace(workspace, workspace_bytes, pl.total)) != GS_SUCCESS) return st;

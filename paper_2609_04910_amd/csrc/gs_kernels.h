@@ -350,8 +350,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 // through one more MFMA against the FCT 16-row tiles of V^T streamed with
 // the keys.  The forward result goes to out_s (M x C, split partials at
 // part_stride_s), exactly as k_fwd would produce it.
+// Two waves per SIMD (at most 256 VGPRs) wherever LDS allows two workgroups
+// per CU: the large-D / large-C instances would otherwise take a few more
+// registers and run one wave per SIMD, which costs far more than the spill
+// of a few values outside the key loop.
 template <typename T, int DP, int CW, int QT, int FCT>
-__global__ __launch_bounds__(kBlockThreads) void k_dq(
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_dq(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
     const uint4* __restrict__ kt_ks, const uint32_t* __restrict__ kslot, const uint4* __restrict__ vs,
