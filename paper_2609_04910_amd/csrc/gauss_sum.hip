@@ -277,14 +277,17 @@ PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel) {
   return ps;
 }
 
-// Largest value width whose forward sum rides along in the dq pass: beyond
-// one 16-row tile of V^T the extra contraction and its registers cost more
-// than a separate forward pass.
+// When the forward sum rides along in the dq pass.  C = 1 always (it is the
+// row sum the gradient forms anyway).  Otherwise only while it needs a single
+// 16-row tile of V^T and D <= 128: beyond that the extra contraction and its
+// registers cost more than a separate forward pass (C = 128: 0.52 ms fused
+// against 0.17 + 0.25 ms; D = 256, C = 16: 598 ms against 112 + 388 ms).
 constexpr int64_t kFuseMaxC = 16;
+constexpr int64_t kFuseMaxD = 128;
 
 struct Want {
   bool fwd = false, dq = false, dk = false, dv = false;
-  bool fuse = false;                           // set by want_for: C <= kFuseMaxC
+  bool fuse = false;  // set by want_for (kFuseMaxC, kFuseMaxD)
   bool fused() const { return fwd && dq && fuse; }  // forward computed inside the dq pass
 };
 
@@ -294,7 +297,7 @@ Want want_for(const gs_problem& p, bool fwd, bool dq, bool dk, bool dv) {
   w.dq = dq;
   w.dk = dk;
   w.dv = dv;
-  w.fuse = p.C <= kFuseMaxC;
+  w.fuse = p.C == 1 || (p.C <= kFuseMaxC && p.D <= kFuseMaxD);
   return w;
 }
 

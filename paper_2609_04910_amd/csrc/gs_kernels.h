@@ -118,9 +118,14 @@ __device__ __forceinline__ void key_stream(int s_begin, int s_end, Issue issue, 
   }
 }
 
-// Stages for a step of `stage_bytes`: three when they fit in 160 KiB of LDS
-// and the per-step load count fits the vmcnt field, else two.
+// Stages for a step of `stage_bytes`: three when two workgroups per CU still
+// fit in 160 KiB of LDS (and the per-step load count fits the vmcnt field),
+// else two if that keeps two workgroups per CU (a second resident workgroup
+// is worth more than the deeper prefetch: the D = 256 gradient runs 1.5x
+// faster), else three, else two.
 constexpr int ring_stages(int stage_bytes, int loads) {
+  if (3 * stage_bytes <= 80 * 1024 && loads < 64) return 3;
+  if (2 * stage_bytes <= 80 * 1024) return 2;
   return (3 * stage_bytes <= 160 * 1024 && loads < 64) ? 3 : 2;
 }
 
