@@ -194,7 +194,7 @@ struct Side {  // one point set with the arrays derived from it
   uint16_t* rt = nullptr;       // RT copy (input dtype)
   float* nh = nullptr;          // -||x||^2/2 (padding rows: kPadBias)
   uint16_t* ks = nullptr;       // KS fp16 copy (operand of sum_n P k_n) as keys of a gradient pass
-  uint16_t* samp_rt = nullptr;  // 64 sampled rows, RT layout
+  uint16_t* samp_rt = nullptr;  // kSampleRows sampled rows, RT layout (coarse sample first)
   float* samp_nh = nullptr;     // their half norms
 };
 
@@ -328,24 +328,26 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   const bool keys_k = w.fwd || w.dq;  // passes whose keys are k
   const bool keys_q = w.dk || w.dv;   // passes whose keys are q
   const bool need_k_ks = w.dq, need_q_ks = w.dk;
-  auto side = [&](Side& s, int64_t n_pad, bool ks, bool sample) {
+  // sample of a key side: its half norms are followed by the row-bound flags
+  // of the rows queried against it (the other side's padded row count)
+  auto side = [&](Side& s, int64_t n_pad, bool ks, bool sample, int64_t other_pad) {
     s.rt = cv.take<uint16_t>(n_pad * W * 2);
     s.nh = cv.take<float>(n_pad * 4);
     if (ks) s.ks = cv.take<uint16_t>(n_pad * W * 2);
     if (sample) {
-      s.samp_rt = cv.take<uint16_t>(64 * W * 2);
-      s.samp_nh = cv.take<float>(64 * 4);
+      s.samp_rt = cv.take<uint16_t>(kSampleRows * W * 2);
+      s.samp_nh = cv.take<float>(kSampleRows * 4 + other_pad * 4);
     }
   };
   if (alias) {
     // single channel: the KS copies carry the signs of v (dq) or dout (dk)
     const bool two = p.C == 1 && need_q_ks && need_k_ks;
-    side(pl.q, pl.Mp, need_q_ks || need_k_ks, true);
+    side(pl.q, pl.Mp, need_q_ks || need_k_ks, true, pl.Mp);
     pl.k = pl.q;
     if (two) pl.k.ks = cv.take<uint16_t>(pl.Mp * W * 2);
   } else {
-    side(pl.q, pl.Mp, need_q_ks, keys_q);
-    side(pl.k, pl.Np, need_k_ks, keys_k);
+    side(pl.q, pl.Mp, need_q_ks, keys_q, pl.Np);
+    side(pl.k, pl.Np, need_k_ks, keys_k, pl.Mp);
   }
   if (keys_k) pl.scal_kv = cv.take<float>(pl.Np * 2 * 4);
   if (keys_q) pl.scal_qg = cv.take<float>(pl.Mp * 2 * 4);
@@ -432,7 +434,7 @@ void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t n, int64_t n_pad, 
   hipLaunchKernelGGL(k_points_rt_norm<T>, dim3(grid1(n_pad * (W / 8))), dim3(256), 0, c.st, x16, n,
                      (int)p.D, n_pad, W, s.rt, s.nh);
   if (s.samp_rt)
-    hipLaunchKernelGGL(k_sample<T>, dim3(grid1(64 * W)), dim3(256), 0, c.st, x16, n, (int)p.D, W,
+    hipLaunchKernelGGL(k_sample<T>, dim3(grid1(kSampleRows * W)), dim3(256), 0, c.st, x16, n, (int)p.D, W,
                        s.samp_rt, s.samp_nh);
   if (s.ks) {
     const uint32_t* sl = nullptr;
@@ -493,6 +495,29 @@ void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64
   const bool vals = c.p->C == 1 && x != nullptr;
   hipLaunchKernelGGL(k_step_scalars, dim3(grid1(n_pad * 2)), dim3(256), 0, c.st, (const float*)s.nh,
                      vals ? x : nullptr, (int)dt, n, n_pad, slot, c.tau2, out);
+}
+
+// Row-bound flags of the rows of `qs` (n rows, n_pad padded) against the
+// sampled keys of `ks`, stored after the sample's half norms.
+template <typename T>
+void row_check_t(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Side& ks) {
+  uint32_t* shift = reinterpret_cast<uint32_t*>(ks.samp_nh + kSampleRows);
+  const dim3 grid((unsigned)(n_pad / 256)), block(kBlockThreads);
+  const uint4* q = (const uint4*)qs.rt;
+  const uint4* s = (const uint4*)ks.samp_rt;
+  switch (c.pl->dm.DP) {
+    case 1: hipLaunchKernelGGL((k_row_check<T, 1>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
+    case 2: hipLaunchKernelGGL((k_row_check<T, 2>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
+    case 4: hipLaunchKernelGGL((k_row_check<T, 4>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
+    case 8: hipLaunchKernelGGL((k_row_check<T, 8>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
+  }
+}
+
+void row_check(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Side& ks) {
+  if (c.p->qk_dtype == GS_F16)
+    row_check_t<F16>(c, qs, n, n_pad, ks);
+  else
+    row_check_t<BF16>(c, qs, n, n_pad, ks);
 }
 
 void combine(const Ctx& c, const PassShape& ps, int64_t count, float* out) {
@@ -751,6 +776,9 @@ gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, 
   if (pl.scal_kv) prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
   if (pl.scal_qg) prep_scalars(c, pl.q, dout, dout_dtype, M, pl.Mp, pl.slots + 1, pl.scal_qg);
   const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
+  // full-sample row-bound flags for the forward-kernel passes (fwd, dv)
+  if (w.fwd && !w.fused()) row_check(c, pl.q, M, pl.Mp, pl.k);
+  if (w.dv && !(alias && w.fwd && !w.fused())) row_check(c, pl.k, N, pl.Np, pl.q);
   if (w.fwd && !w.fused()) pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out);
   if (w.dq)
     pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1,

@@ -44,6 +44,8 @@ constexpr int kBlockThreads = kWave * kWavesPerBlock;
 constexpr int kStep = 32;      // keys per inner step
 constexpr int kRowPad = 256;   // row padding of every point / value array
 constexpr float kPadBias = -1.0e30f;  // -||k||^2/2 of a padding row: Phi = 0
+constexpr int kSampleCoarse = 64;     // keys of the first row-bound check
+constexpr int kSampleRows = 1024;     // keys of the second (and all sampled rows)
 
 struct F16 {
   typedef _Float16 storage;

@@ -20,8 +20,9 @@
 // Nothing of size M x N is ever stored.
 //
 // Range: kernel values are fp16 numbers in [0, 1].  When every row maximum of
-// the wave's queries over a fixed sample of 64 keys is at least 2^-8 the
-// offset off_m is 0; otherwise the wave first walks its keys once to find the
+// the wave's queries over a fixed sample of keys (64 keys; the forward also
+// 1024, via k_row_check) is at least 2^-8 the offset off_m is 0; otherwise
+// the wave first walks its keys once to find the
 // exact row maximum of the exponent and uses it as off_m (so the largest value
 // of every row is 1 and fp16 keeps full relative precision for all values
 // within 2^-14 of it); the epilogue multiplies by 2^off_m.  Values and
@@ -36,7 +37,6 @@ namespace gs {
 // Waves whose sampled row maximum of the log2 kernel value falls below this
 // evaluate the row maxima exactly first.
 constexpr float kShiftBelow = -8.0f;
-constexpr int kSampleKeys = 64;        // keys in the row-bound sample (2 steps)
 constexpr int kScalarFloats = 64;      // per step: 32 half norms, 32 scaled C = 1 values
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -154,9 +154,12 @@ __device__ __forceinline__ void load_k_tile(const uint4* base, int64_t tile, int
   for (int dc = 0; dc < DP; ++dc) kr[dc] = base[((tile * DP + dc) * 16 + j) * 4 + g];
 }
 
-// Per-wave prologue: query operands, biases, and the offset decision.
-//   sample_rt / sample_nh: 64 sampled keys of the key set (RT layout, half norms)
-// Returns in off[] 0, or (when needed) a marker to compute exact maxima.
+// Per-wave prologue: the coarse row-bound check.  sample_rt / sample_nh: the
+// sampled keys (RT layout, half norms, coarse sample first).  Returns whether
+// some query of the wave has its sampled row maximum of the log2 kernel value
+// below kShiftBelow over the coarse sample.  The forward kernel then consults
+// the full-sample flags of k_row_check; the gradient kernel takes the exact
+// row maxima right away (a clustered key set only costs it time).
 template <typename T, int DP, int QT>
 __device__ __forceinline__ bool needs_shift(const uint4* __restrict__ sample_rt,
                                             const float* __restrict__ sample_nh,
@@ -166,7 +169,7 @@ __device__ __forceinline__ bool needs_shift(const uint4* __restrict__ sample_rt,
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) smax[qt] = -__builtin_inff();
 #pragma unroll
-  for (int t = 0; t < kSampleKeys / 16; ++t) {
+  for (int t = 0; t < kSampleCoarse / 16; ++t) {
     uint4 kr[DP];
     load_k_tile<DP>(sample_rt, t, j, g, kr);
     const floatx4 cin = *reinterpret_cast<const floatx4*>(sample_nh + 16 * t + 4 * g);
@@ -180,6 +183,75 @@ __device__ __forceinline__ bool needs_shift(const uint4* __restrict__ sample_rt,
     low |= (q0 + 16 * qt + j < M) && (L < kShiftBelow);
   }
   return __any(low);
+}
+
+// Row-bound check, one flag per query row: shift[m] = 1 when the largest
+// log2 kernel value of row m over the sampled keys (sample_rt / sample_nh: RT
+// layout and half norms, coarse sample first) is below kShiftBelow, i.e. the
+// row needs its exact maximum as offset.  A wave takes 64 rows; it checks the
+// coarse sample first and scans the full one only when some row fails (a
+// clustered key set can hide a row's own cluster from a small sample; the
+// full-sample maximum is never below the coarse one, so rows passing the
+// coarse check pass the full one).  The forward kernel reads these flags.
+template <typename T, int DP>
+__global__ __launch_bounds__(kBlockThreads) void k_row_check(
+    const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ sample_rt,
+    const float* __restrict__ sample_nh, float tau2, int64_t M, uint32_t* __restrict__ shift) {
+  constexpr int QT = 4;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int j = lane & 15, g = lane >> 4;
+  const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave) * (16 * QT);
+  uint4 qreg[QT][DP];
+  float bq[QT], smax[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    load_k_tile<DP>(qs, q0 / 16 + qt, j, g, qreg[qt]);
+    bq[qt] = tau2 * nhq[q0 + 16 * qt + j];
+    smax[qt] = -__builtin_inff();
+  }
+  auto scan = [&](int t0, int t1) {
+    for (int t = t0; t < t1; ++t) {
+      uint4 kr[DP];
+      load_k_tile<DP>(sample_rt, t, j, g, kr);
+      const floatx4 cin = *reinterpret_cast<const floatx4*>(sample_nh + 16 * t + 4 * g);
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
+    }
+  };
+  bool low[QT];
+  auto decide = [&]() {
+    bool any = false;
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      const float L = fmaf(wave_max_over_g(smax[qt]), tau2, bq[qt]);
+      low[qt] = (q0 + 16 * qt + j < M) && (L < kShiftBelow);
+      any |= low[qt];
+    }
+    return __any(any);
+  };
+  scan(0, kSampleCoarse / 16);
+  if (decide()) {
+    scan(kSampleCoarse / 16, kSampleRows / 16);
+    decide();
+  }
+  if (g == 0)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) shift[q0 + 16 * qt + j] = low[qt] ? 1u : 0u;
+}
+
+// The flags of k_row_check for the rows queried against a sample are stored
+// right after that sample's half norms.
+__device__ __forceinline__ const uint32_t* row_flags(const float* sample_nh) {
+  return reinterpret_cast<const uint32_t*>(sample_nh + kSampleRows);
+}
+
+// Whether any of the wave's 16 QT query rows is flagged by k_row_check.
+template <int QT>
+__device__ __forceinline__ bool wave_needs_shift(const uint32_t* __restrict__ shift, int64_t q0, int j) {
+  uint32_t f = 0;
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) f |= shift[q0 + 16 * qt + j];
+  return __any(f != 0);
 }
 
 // Exact row maxima of S~ over the wave's key range, from the RT key copy in
@@ -282,7 +354,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     bq[qt] = tau2 * nhq[q0 + 16 * qt + j];
     off[qt] = 0.0f;
   }
-  if (needs_shift<T, DP, QT>(samp_rt, samp_nh, qreg, bq, tau2, q0, M, j, g))
+  if (needs_shift<T, DP, QT>(samp_rt, samp_nh, qreg, bq, tau2, q0, M, j, g) &&
+      wave_needs_shift<QT>(row_flags(samp_nh), q0, j))
     exact_offsets<T, DP, QT>(ks, scal, qreg, s_begin, s_end, j, g, tau2, bq, off);
 
   floatx4 O[QT][CT];

@@ -157,18 +157,29 @@ __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, in
   }
 }
 
-// Row-bound sample: rows n_j = floor(j N / 64), j < 64, of a point set, in
-// RT layout (64 rows, W columns, input dtype) with their half norms; with
-// N < 64 the rows j < N and padding (zero point, kPadBias norm) after.
+// Row-bound sample of a point set: rows n_j = floor(j N / kSampleRows) for
+// j < kSampleRows (repeats when N is smaller), in RT layout (input dtype) with
+// their half norms.  Stored coarse-first: positions 0 .. kSampleCoarse-1 hold
+// j = 0, 16, 32, ... (the rows floor(i N / kSampleCoarse)), the remaining
+// positions the other j in increasing order, so that the coarse sample is the
+// first kSampleCoarse / 16 RT tiles.
 template <typename T>
 __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W,
                          uint16_t* __restrict__ srt, float* __restrict__ snh) {
+  constexpr int kStride = kSampleRows / kSampleCoarse;
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= 64 * W) return;
-  const int j = t / W, w = t - (t / W) * W;
-  const bool real = n >= 64 || j < n;
-  const int64_t r = n >= 64 ? ((int64_t)j * n) / 64 : j;
-  srt[rt_index(j, w, W)] = (real && w < D) ? x[r * D + w] : (uint16_t)0;
+  if (t >= kSampleRows * W) return;
+  const int pos = t / W, w = t - (t / W) * W;
+  int j;
+  if (pos < kSampleCoarse) {
+    j = kStride * pos;
+  } else {
+    const int q = pos - kSampleCoarse;
+    j = (q / (kStride - 1)) * kStride + q % (kStride - 1) + 1;
+  }
+  const bool real = n > 0;
+  const int64_t r = real ? ((int64_t)j * n) / kSampleRows : 0;
+  srt[rt_index(pos, w, W)] = (real && w < D) ? x[r * D + w] : (uint16_t)0;
   if (w == 0) {
     double acc = 0.0;
     if (real)
@@ -176,7 +187,7 @@ __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W
         double v = (double)T::to_float(x[r * D + d]);
         acc += v * v;
       }
-    snh[j] = real ? (float)(-0.5 * acc) : kPadBias;
+    snh[pos] = real ? (float)(-0.5 * acc) : kPadBias;
   }
 }
 
