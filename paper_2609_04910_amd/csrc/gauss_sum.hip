@@ -51,16 +51,21 @@ inline Dims dims_of(int64_t D, int64_t C) {
   return d;
 }
 
-// Query tiles per wave.  Forward: the largest of 4, 2, 1 whose kernel (as
-// compiled for gfx950) keeps the register count at or below 256 per lane (two
-// waves per SIMD).  Gradient: for D > 64 two tiles even where that needs the
+// Query tiles per wave.  Forward: 8 for D <= 64 with C <= 32 (the per-step
+// barrier, loads and K-tile reads then cover twice the pairs: D = 64, C = 1
+// 0.76 -> 0.71 ms), else the largest of 4, 2, 1 whose kernel (as compiled
+// for gfx950) keeps the register count at or below 256 per lane (two waves
+// per SIMD).  Gradient: for D > 64 two tiles even where that needs the
 // occupancy hint on k_dq or (D = 256, whose LDS ring allows one workgroup per
 // CU anyway) one wave per SIMD: a K tile read from LDS then feeds two MFMAs,
 // and a single tile per wave is bound by LDS bandwidth; D = 256 with
 // C > 128 keeps one tile (two would spill inside the key loop).
 constexpr int fwd_qt(int DP, int CT) {
-  return CT >= 16 ? 1 : CT == 8 ? 2 : (DP == 8 && CT > 1) ? 2 : 4;
+  return CT >= 16 ? 1 : CT == 8 ? 2 : (DP == 8 && CT > 1) ? 2 : (DP <= 2 && CT <= 2) ? 8 : 4;
 }
+// Every workgroup's rows lie inside the padded row range.
+static_assert(kRowPad % (kBlockThreads / 4 * 8) == 0 && kRowPad % 256 == 0, "row padding vs. query tiles");
+
 constexpr int dq_qt(int DP, int CW) {
   return DP >= 4 ? (DP == 8 && CW == 8 ? 1 : 2) : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
 }

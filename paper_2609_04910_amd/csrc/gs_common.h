@@ -42,7 +42,7 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWave * kWavesPerBlock;
 constexpr int kStep = 32;      // keys per inner step
-constexpr int kRowPad = 256;   // row padding of every point / value array
+constexpr int kRowPad = 512;   // row padding of every point / value array (one workgroup of 8-tile waves)
 constexpr float kPadBias = -1.0e30f;  // -||k||^2/2 of a padding row: Phi = 0
 constexpr int kSampleCoarse = 64;     // keys of the first row-bound check
 constexpr int kSampleRows = 1024;     // keys of the second (and all sampled rows)

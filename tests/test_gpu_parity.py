@@ -51,6 +51,10 @@ SHAPES = [
     # row-maximum shift
     (150, 400, 8, 4, "f16", "f32", "f32", 3.0, 3.0),
     (150, 400, 32, 2, "bf16", "f32", "f32", 10.0, 2.0),
+    # row counts that are odd multiples of 256 and ragged beyond 512: the
+    # D <= 64 forward runs 128 query rows per wave, 512 per workgroup
+    (768, 777, 64, 1, "f16", "f32", "f32", None, 1.0),
+    (1300, 600, 32, 3, "bf16", "f32", "f32", None, 1.0),
 ]
 
 
