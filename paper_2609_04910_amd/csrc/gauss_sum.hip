@@ -439,8 +439,8 @@ void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t n, int64_t n_pad, 
   hipLaunchKernelGGL(k_points_rt_norm<T>, dim3(grid1(n_pad * (W / 8))), dim3(256), 0, c.st, x16, n,
                      (int)p.D, n_pad, W, s.rt, s.nh);
   if (s.samp_rt)
-    hipLaunchKernelGGL(k_sample<T>, dim3(grid1(kSampleRows * W)), dim3(256), 0, c.st, x16, n, (int)p.D, W,
-                       s.samp_rt, s.samp_nh);
+    hipLaunchKernelGGL(k_sample, dim3(grid1(kSampleRows * W)), dim3(256), 0, c.st, x16, n, (int)p.D, W,
+                       (const float*)s.nh, s.samp_rt, s.samp_nh);
   if (s.ks) {
     const uint32_t* sl = nullptr;
     if (p.qk_dtype == GS_BF16) {

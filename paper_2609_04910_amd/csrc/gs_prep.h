@@ -36,6 +36,14 @@ __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
   uint32_t mb = 0;
+  // four independent loads in flight per thread
+  for (; i + 3 * stride < count; i += 4 * stride) {
+    uint32_t b[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) b[u] = __builtin_bit_cast(uint32_t, fabsf(load_any(x, i + u * stride, dtype)));
+#pragma unroll
+    for (int u = 0; u < 4; ++u) mb = b[u] > mb ? b[u] : mb;
+  }
   for (; i < count; i += stride) {
     uint32_t b = __builtin_bit_cast(uint32_t, fabsf(load_any(x, i, dtype)));
     mb = b > mb ? b : mb;
@@ -162,10 +170,11 @@ __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, in
 // their half norms.  Stored coarse-first: positions 0 .. kSampleCoarse-1 hold
 // j = 0, 16, 32, ... (the rows floor(i N / kSampleCoarse)), the remaining
 // positions the other j in increasing order, so that the coarse sample is the
-// first kSampleCoarse / 16 RT tiles.
-template <typename T>
+// first kSampleCoarse / 16 RT tiles.  nh: the half norms of the point set
+// (k_points_rt_norm), copied so that sampled and streamed keys agree exactly.
 __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W,
-                         uint16_t* __restrict__ srt, float* __restrict__ snh) {
+                         const float* __restrict__ nh, uint16_t* __restrict__ srt,
+                         float* __restrict__ snh) {
   constexpr int kStride = kSampleRows / kSampleCoarse;
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= kSampleRows * W) return;
@@ -180,15 +189,7 @@ __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W
   const bool real = n > 0;
   const int64_t r = real ? ((int64_t)j * n) / kSampleRows : 0;
   srt[rt_index(pos, w, W)] = (real && w < D) ? x[r * D + w] : (uint16_t)0;
-  if (w == 0) {
-    double acc = 0.0;
-    if (real)
-      for (int d = 0; d < D; ++d) {
-        double v = (double)T::to_float(x[r * D + d]);
-        acc += v * v;
-      }
-    snh[pos] = real ? (float)(-0.5 * acc) : kPadBias;
-  }
+  if (w == 0) snh[pos] = real ? nh[r] : kPadBias;  // the row's own half norm (same value)
 }
 
 // Per-step key scalars, 64 floats (256 bytes) per 32-key step:
@@ -228,7 +229,8 @@ __global__ void k_step_scalars(const float* __restrict__ nh, const void* __restr
 }
 
 // out[m, w] = sum_s part[s, m, w] in split order (deterministic); four
-// elements per thread where count allows 16-byte accesses.
+// elements per thread where count allows 16-byte accesses, the loads of up to
+// eight splits issued together before they are added in order.
 __global__ void k_combine(const float* __restrict__ part, int splits, int64_t count,
                           float* __restrict__ out) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -238,12 +240,19 @@ __global__ void k_combine(const float* __restrict__ part, int splits, int64_t co
     const float4* p4 = reinterpret_cast<const float4*>(part);
     for (; i < c4; i += stride) {
       float4 acc = p4[i];
-      for (int s = 1; s < splits; ++s) {
-        const float4 v = p4[(int64_t)s * c4 + i];
-        acc.x += v.x;
-        acc.y += v.y;
-        acc.z += v.z;
-        acc.w += v.w;
+      for (int s0 = 1; s0 < splits; s0 += 8) {
+        float4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (s0 + u < splits) v[u] = p4[(int64_t)(s0 + u) * c4 + i];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (s0 + u < splits) {
+            acc.x += v[u].x;
+            acc.y += v[u].y;
+            acc.z += v[u].z;
+            acc.w += v[u].w;
+          }
       }
       reinterpret_cast<float4*>(out)[i] = acc;
     }
@@ -251,7 +260,15 @@ __global__ void k_combine(const float* __restrict__ part, int splits, int64_t co
   }
   for (; i < count; i += stride) {
     float acc = part[i];
-    for (int s = 1; s < splits; ++s) acc += part[(int64_t)s * count + i];
+    for (int s0 = 1; s0 < splits; s0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < splits) v[u] = part[(int64_t)(s0 + u) * count + i];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < splits) acc += v[u];
+    }
     out[i] = acc;
   }
 }
