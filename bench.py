@@ -222,6 +222,9 @@ def main():
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--flow", action="store_true",
+                    help="mmd_flow: time one gauss_sum_mmd_flow call per step (s, the flow field "
+                         "and MMD^2 = v^T s) instead of gauss_sum_fwd_bwd")
     ap.add_argument("--separate", action="store_true",
                     help="time separate gauss_sum_fwd + gauss_sum_bwd calls instead of one "
                          "gauss_sum_fwd_bwd call")
@@ -267,17 +270,24 @@ def main():
     g = t(w.g) if w.g is not None else None
     grads = tuple(p in passes for p in ("dq", "dk", "dv"))
     do_fwd = "fwd" in passes
+    if args.flow and args.workload != "mmd_flow":
+        print("--flow applies to the mmd_flow workload only", file=sys.stderr)
+        sys.exit(2)
     fused = do_fwd and any(grads) and not args.separate
     qk_code = gs.GS_F16 if w.qk_dtype == "f16" else gs.GS_BF16
     v_code = {np.dtype(np.float32): gs.GS_F32, np.dtype(np.float16): gs.GS_F16}[w.v.dtype]
     ws_f = gs.gauss_sum_fwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code) if do_fwd else 0
     ws_b = gs.gauss_sum_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if any(grads) else 0
     ws_fb = gs.gauss_sum_fwd_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if fused else 0
-    ws = torch.empty(max(ws_f, ws_b, ws_fb, 1), dtype=torch.uint8, device=dev)
+    ws_fl = gs.gauss_sum_mmd_flow_workspace_size(w.N, w.D, qk_code, v_code) if args.flow else 0
+    ws = torch.empty(max(ws_f, ws_b, ws_fb, ws_fl, 1), dtype=torch.uint8, device=dev)
     out = torch.empty((w.M, w.C), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
+        if args.flow:
+            gs.gauss_sum_mmd_flow(q, v, float(w.tau), workspace=ws, stream=stream)
+            return
         if fused:
             gs.gauss_sum_fwd_bwd(q, k, v, float(w.tau), g, want=grads, out=out, workspace=ws,
                                  stream=stream)
@@ -358,7 +368,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": describe(w, passes), "M": w.M, "N": w.N, "D": w.D, "C": w.C,
                    "tau": float(w.tau), "passes": "+".join(passes),
-                   "api": "gauss_sum_fwd_bwd" if fused else
+                   "api": "gauss_sum_mmd_flow" if args.flow else "gauss_sum_fwd_bwd" if fused else
                           "+".join(n for n, u in (("gauss_sum_fwd", do_fwd),
                                                   ("gauss_sum_bwd", any(grads))) if u)},
         "mfma_frac_of_peak": step_flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16,

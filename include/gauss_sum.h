@@ -124,6 +124,29 @@ gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, c
 /* Bytes of device workspace gauss_sum_fwd_bwd needs (0 if p is invalid). */
 size_t gauss_sum_fwd_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv);
 
+/* One MMD-flow evaluation (Sec. 3, the MMD and particle-flow paragraphs):
+ * points x (N x D, qk_dtype) serve as both queries and keys, v (N x 1,
+ * v_dtype) are the signed weights of sigma = mu - nu = sum_n v_n delta_{x_n}.
+ * Writes, for m < N,
+ *   s[m]       = sum_n Phi(x_m, x_n) v_n                      (fp32, N x 1)
+ *   grad[m, :] = tau (sum_n Phi v_n x_n - x_m s[m])           (fp32, N x D)
+ *              = the gradient of s_m with respect to its query point x_m
+ *                (the MMD-flow / SVGD kernel-term velocity),
+ *   *mmd2      = sum_m v_m s[m] = MMD_tau(mu, nu)^2            (fp64 scalar)
+ * from one pass over the pairs (the forward sum is the gradient pass's own
+ * row sum); the inner product is a fixed-order fp64 reduction, so *mmd2 is
+ * bitwise reproducible.  Any of s, grad, mmd2 may be NULL (not wanted); at
+ * least one must be given.  All pointers are device pointers; mmd2 points to
+ * one double (8-byte aligned).  Requires p->M == p->N (GS_ERR_BAD_SHAPE) and
+ * p->C == 1 (GS_ERR_UNSUPPORTED); other checks as gauss_sum_fwd_bwd.  N == 0
+ * writes *mmd2 = 0.  Workspace: gauss_sum_mmd_flow_workspace_size. */
+gs_status gauss_sum_mmd_flow(const gs_problem* p, const void* x, const void* v, float tau, float* s,
+                             float* grad, double* mmd2, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* Bytes of device workspace gauss_sum_mmd_flow needs (0 if p is invalid for it). */
+size_t gauss_sum_mmd_flow_workspace_size(const gs_problem* p);
+
 /* Static, never-NULL description of a status code. */
 const char* gauss_sum_status_string(gs_status s);
 

@@ -634,9 +634,22 @@ gs_status launch_status() {
 
 using namespace gs;
 
+namespace {
+constexpr int kDotBlocks = 256;
+
+// Leading workspace of gauss_sum_mmd_flow: all-ones upstream gradient (n
+// fp32), the forward sum when the caller does not want it (n fp32), the
+// reduction partials; the gradient pass's own workspace follows.
+size_t flow_extra(int64_t n) {
+  const int64_t a = gs::round_up(std::max<int64_t>(n, 1) * 4, 256);
+  return (size_t)(2 * a + gs::round_up(kDotBlocks * 8, 256));
+}
+}  // namespace
+
 extern "C" {
 
 int gauss_sum_abi_version(void) { return GAUSS_SUM_ABI_VERSION; }
+
 
 const char* gauss_sum_status_string(gs_status s) {
   switch (s) {
@@ -859,4 +872,61 @@ gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, c
   }
 }
 
+size_t gauss_sum_mmd_flow_workspace_size(const gs_problem* p) {
+  if (!p || gs::check_problem(p) != GS_SUCCESS || p->M != p->N || p->C != 1) return 0;
+  return flow_extra(p->N) + gs::workspace_for(p, true, 1, 0, 0);
+}
+
+gs_status gauss_sum_mmd_flow(const gs_problem* p, const void* x, const void* v, float tau, float* s,
+                             float* grad, double* mmd2, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  using namespace gs;
+  try {
+    gs_status st = check_problem(p);
+    if (st != GS_SUCCESS) return st;
+    if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+    if (p->M != p->N) return GS_ERR_BAD_SHAPE;
+    if (p->C != 1) return GS_ERR_UNSUPPORTED;
+    if (!s && !grad && !mmd2) return GS_ERR_NULL_POINTER;
+    const int64_t n = p->N, D = p->D;
+    if (n > 0 && (!x || !v)) return GS_ERR_NULL_POINTER;
+    if (!aligned(mmd2, 8) || !aligned(s, 4) || !aligned(grad, 4)) return GS_ERR_MISALIGNED;
+    const size_t need = gauss_sum_mmd_flow_workspace_size(p);
+    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_SUCCESS) return st;
+    // outputs overlap neither the inputs, the workspace nor each other (all
+    // checked before anything is enqueued)
+    const Range in[3] = {range_of(x, n * D * 2), range_of(v, n * (int64_t)dsize(p->v_dtype)),
+                         range_of(workspace, (int64_t)need)};
+    const Range outs[3] = {range_of(s, s ? n * 4 : 0), range_of(grad, grad ? n * D * 4 : 0),
+                           range_of(mmd2, mmd2 ? 8 : 0)};
+    for (int a = 0; a < 3; ++a) {
+      for (int b = 0; b < 3; ++b)
+        if (overlap(outs[a], in[b])) return GS_ERR_ALIAS;
+      for (int b = a + 1; b < 3; ++b)
+        if (overlap(outs[a], outs[b])) return GS_ERR_ALIAS;
+    }
+    char* base = static_cast<char*>(workspace);
+    const int64_t a = round_up(std::max<int64_t>(n, 1) * 4, 256);
+    float* ones = reinterpret_cast<float*>(base);
+    float* sbuf = reinterpret_cast<float*>(base + a);
+    double* parts = reinterpret_cast<double*>(base + 2 * a);
+    const size_t extra = flow_extra(n);
+    float* s_out = s ? s : (mmd2 ? sbuf : nullptr);
+    if (n > 0) {
+      if (grad) hipLaunchKernelGGL(k_fill_f32, dim3(grid1(n)), dim3(256), 0, stream, ones, n, 1.0f);
+      st = run(p, x, x, v, tau, grad ? ones : nullptr, GS_F32, s_out, grad, nullptr, nullptr,
+               base + extra, workspace_bytes - extra, stream);
+      if (st != GS_SUCCESS) return st;
+    }
+    if (mmd2) {
+      hipLaunchKernelGGL(k_dot_partial, dim3(kDotBlocks), dim3(256), 0, stream, v, (int)p->v_dtype,
+                         (const float*)s_out, n, parts);
+      hipLaunchKernelGGL(k_dot_final, dim3(1), dim3(64), 0, stream, (const double*)parts, kDotBlocks,
+                         mmd2);
+    }
+    return launch_status();
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
 }  // extern "C"

@@ -228,6 +228,33 @@ __global__ void k_step_scalars(const float* __restrict__ nh, const void* __restr
   }
 }
 
+// Inner product sum_m v_m s_m in fp64, fixed order: workgroup b sums the
+// elements b*256 + t + k*gridDim*256 of thread t in index order, then a
+// fixed tree over its threads; k_dot_final adds the workgroup partials in
+// index order.  So the result does not depend on timing.
+__global__ void k_dot_partial(const void* __restrict__ v, int dtype, const float* __restrict__ s,
+                              int64_t n, double* __restrict__ part) {
+  __shared__ double red[256];
+  double acc = 0.0;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    acc += (double)load_any(v, i, dtype) * (double)s[i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[blockIdx.x] = red[0];
+}
+
+__global__ void k_dot_final(const double* __restrict__ part, int parts, double* __restrict__ out) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  double acc = 0.0;
+  for (int b = 0; b < parts; ++b) acc += part[b];
+  *out = acc;
+}
+
 // out[m, w] = sum_s part[s, m, w] in split order (deterministic); four
 // elements per thread where count allows 16-byte accesses, the loads of up to
 // eight splits issued together before they are added in order.

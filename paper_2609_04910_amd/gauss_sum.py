@@ -30,7 +30,7 @@ STATUS = {
 EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_bwd", "gauss_sum_fwd_workspace_size",
             "gauss_sum_bwd_workspace_size", "gauss_sum_fwd_bwd_workspace_size",
             "gauss_sum_status_string", "gauss_sum_abi_version", "gauss_sum_profile_start",
-            "gauss_sum_profile_stop")
+            "gauss_sum_profile_stop", "gauss_sum_mmd_flow", "gauss_sum_mmd_flow_workspace_size")
 PROFILE_FWD, PROFILE_GRAD = 1, 2
 
 
@@ -73,6 +73,10 @@ def load(path=LIB_PATH):
     lib.gauss_sum_fwd_bwd.restype = ctypes.c_int
     lib.gauss_sum_fwd_bwd_workspace_size.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
     lib.gauss_sum_fwd_bwd_workspace_size.restype = sz
+    lib.gauss_sum_mmd_flow.argtypes = [P, vp, vp, ctypes.c_float, f32p, f32p, vp, vp, sz, vp]
+    lib.gauss_sum_mmd_flow.restype = ctypes.c_int
+    lib.gauss_sum_mmd_flow_workspace_size.argtypes = [P]
+    lib.gauss_sum_mmd_flow_workspace_size.restype = sz
     lib.gauss_sum_status_string.argtypes = [ctypes.c_int]
     lib.gauss_sum_status_string.restype = ctypes.c_char_p
     lib.gauss_sum_abi_version.argtypes = []
@@ -250,6 +254,38 @@ def gauss_sum_fwd_bwd(q, k, v, tau, dout, want=(True, True, True), out=None, wor
     if st != 0:
         raise GaussSumError(st, "gauss_sum_fwd_bwd")
     return out, dq, dk, dv
+
+
+def gauss_sum_mmd_flow_workspace_size(N, D, qk_dtype=GS_F16, v_dtype=GS_F32):
+    p = make_problem(N, N, D, 1, qk_dtype, v_dtype)
+    return int(load().gauss_sum_mmd_flow_workspace_size(ctypes.byref(p)))
+
+
+def gauss_sum_mmd_flow(x, v, tau, want=(True, True, True), workspace=None, stream=None):
+    """One MMD-flow evaluation for points x (N x D) and signed weights v (N x 1):
+    (s, grad, mmd2) with s = K v, grad[m] = tau (sum_n Phi v_n x_n - x_m s_m)
+    and mmd2 = v^T s (a 0-d fp64 tensor); None where not wanted."""
+    import torch
+    _check_inputs(x, x, v)
+    N, D = x.shape
+    if v.shape != (N, 1):
+        raise ValueError("v must be N x 1")
+    p = make_problem(N, N, D, 1, _dtype_code(x.dtype), _dtype_code(v.dtype))
+    lib = load()
+    dev = x.device
+    s = torch.empty((N, 1), dtype=torch.float32, device=dev) if want[0] else None
+    grad = torch.empty((N, D), dtype=torch.float32, device=dev) if want[1] else None
+    mmd2 = torch.empty((), dtype=torch.float64, device=dev) if want[2] else None
+    need = int(lib.gauss_sum_mmd_flow_workspace_size(ctypes.byref(p)))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, dev)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_mmd_flow(ctypes.byref(p), _ptr(x), _ptr(v), float(tau), _ptr(s), _ptr(grad),
+                                _ptr(mmd2), _ptr(workspace), wbytes, _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_mmd_flow")
+    return s, grad, mmd2
 
 
 def _make_autograd():

@@ -109,6 +109,26 @@ def test_fwd_bwd_validation(kw, status):
     assert _fb(**kw) == status
 
 
+def _flow(M=8, N=8, D=4, C=1, x=FAKE, v=FAKE + 0x20000, tau=1.0, s=FAKE + 0x30000,
+          grad=FAKE + 0x40000, mmd2=FAKE + 0x50000, ws=FAKE + 0x100000, wsb=1 << 40, p=True):
+    lib = gs.load()
+    prob = gs.make_problem(M, N, D, C, gs.GS_F16, gs.GS_F32)
+    pp = ctypes.byref(prob) if p else None
+    return lib.gauss_sum_mmd_flow(pp, x, v, ctypes.c_float(tau), s, grad, mmd2, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(p=False), 1), (dict(s=None, grad=None, mmd2=None), 1), (dict(x=None), 1),
+    (dict(v=None), 1),
+    (dict(N=9), 2), (dict(D=0), 2), (dict(C=2), 4), (dict(tau=0.0), 3),
+    (dict(mmd2=FAKE + 0x50004), 5), (dict(s=FAKE + 0x30002), 5), (dict(wsb=64), 6), (dict(ws=None), 6),
+    (dict(s=FAKE + 0x10), 9), (dict(grad=FAKE + 0x20000), 9), (dict(mmd2=FAKE + 0x30010), 9),
+    (dict(mmd2=FAKE + 0x100100), 9), (dict(grad=FAKE + 0x30000), 9),
+])
+def test_mmd_flow_validation(kw, status):
+    assert _flow(**kw) == status
+
+
 def test_empty_query_set_is_a_noop():
     # M = 0: nothing to compute; no pointer is touched and no kernel runs.
     assert _fwd(M=0, q=None, out=None) == 0
@@ -131,6 +151,9 @@ def test_workspace_sizes():
     assert gs.gauss_sum_fwd_bwd_workspace_size(1000, 3000, 64, 4, want_dq=False, want_dk=False,
                                                want_dv=False) == \
         gs.gauss_sum_fwd_workspace_size(1000, 3000, 64, 4)
+    flow = gs.gauss_sum_mmd_flow_workspace_size(5000, 64)
+    assert flow > gs.gauss_sum_fwd_bwd_workspace_size(5000, 5000, 64, 1, want_dk=False, want_dv=False)
+    assert flow % 256 == 0
 
 
 def test_profile_hook_arguments():
@@ -150,3 +173,4 @@ def test_no_device_reports_hip_error():
     assert _fwd() == 7
     assert _bwd() == 7
     assert _fb() == 7
+    assert _flow() == 7
