@@ -207,6 +207,90 @@ def cpu_baseline(w, passes, budget_s=15.0):
     }
 
 
+def bench_batched(args):
+    """Batched forward (the paper's benchmark layout): one gauss_sum_fwd_batched
+    call per step over B independent clouds; pairs/s counts B M N per step."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2609_04910_amd import gauss_sum as gs
+    from paper_2609_04910_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    cfg = wl.BATCHED[args.workload]
+    q, k, v, tau = wl.make_batch(args.workload, seed=0)
+    B, M, D = q.shape
+    N, C = v.shape[1], v.shape[2]
+    tq, tk, tv = (torch.from_numpy(a).to(dev) for a in (q, k, v))
+    p_ws = gs.gauss_sum_fwd_workspace_size(M, N, D, C, gs.GS_F16, gs.GS_F32)
+    ws = torch.empty(max(p_ws, 1), dtype=torch.uint8, device=dev)
+    out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gs.gauss_sum_fwd_batched(tq, tk, tv, float(tau), out=out, workspace=ws, stream=stream)
+
+    settle_steps, t0 = 0, time.perf_counter()
+    while settle_steps == 0 or (time.perf_counter() - t0) * 1e3 < args.settle_ms:
+        step()
+        settle_steps += 1
+        torch.cuda.synchronize()
+    settle_ms = (time.perf_counter() - t0) * 1e3
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    cap = args.steps * B
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    gs.gauss_sum_profile_start(cap, gs.PROFILE_FWD)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    kernel_ms = gs.gauss_sum_profile_stop(cap)
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    pairs = float(B) * M * N
+    per_launch = float(M) * N * (2 * D + 2 * C)
+    avg = float(np.mean(kernel_ms)) if kernel_ms else float("nan")
+    achieved = per_launch / (avg * 1e-3) / 1e12
+    res = {
+        "metric": METRIC, "value": pairs / (ms_per_step * 1e-3), "unit": "pairs/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "settle": {"ms": settle_ms, "steps": settle_steps},
+        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+        "config": {"workload": "%s: B=%d independent clouds, M=N=%d, D=%d, C=%d, f16 points "
+                               "N(0, I/D), tau=1, forward" % (args.workload, B, M, D, C),
+                   "B": B, "M": M, "N": N, "D": D, "C": C, "tau": float(tau), "passes": "fwd",
+                   "api": "gauss_sum_fwd_batched"},
+        "mfma_frac_of_peak": pairs * (2 * D + 2 * C) / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
+        "roofline": {"bound": "mfma", "kernel": "k_fwd", "achieved": achieved,
+                     "peak": PEAK_MFMA_F16 / 1e12, "unit": "TFLOP/s",
+                     "frac": achieved / (PEAK_MFMA_F16 / 1e12),
+                     "traffic": recorded_traffic(args.workload, "k_fwd"), "avg_launch_ms": avg,
+                     "launches": len(kernel_ms), "flops_per_launch": per_launch,
+                     "launch_share_of_step": avg * B / ms_per_step},
+    }
+    if not args.no_cpu:
+        threads = min(oracle.default_threads(), 16)
+        oracle.fwd(q[0], k[0], v[0], float(tau), rows=np.arange(1), threads=threads)
+        rows = np.arange(64)
+        t = time.perf_counter()
+        oracle.fwd(q[0], k[0], v[0], float(tau), rows=rows, threads=threads)
+        t = time.perf_counter() - t
+        n_rows = int(min(M, max(64, 64 * args.cpu_budget / max(t, 1e-3))))
+        rows = np.sort(np.random.default_rng(3).choice(M, size=n_rows, replace=False))
+        t = time.perf_counter()
+        oracle.fwd(q[0], k[0], v[0], float(tau), rows=rows, threads=threads)
+        t = time.perf_counter() - t
+        res["cpu_baseline"] = {"value": n_rows * N / t, "unit": "pairs/s", "cores": threads,
+                               "kind": "oracle",
+                               "sample": "fp64 oracle, forward on %d of %d query rows of problem 0, "
+                                         "each against all %d keys, %.1f s" % (n_rows, M, N, t)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -218,7 +302,7 @@ def main():
                     help="also run a device copy of MIB MiB (counter calibration for --traffic-from)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="record roofline traffic from two rocprofv3 --pmc csv outputs and exit")
-    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES))
+    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32"])
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -252,6 +336,9 @@ def main():
     gs.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.workload in wl.BATCHED:
+        bench_batched(args)
+        return
 
     passes = PASSES[args.workload]
     tau = args.tau if args.workload == "mixture_d32" else None

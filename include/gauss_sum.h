@@ -124,6 +124,37 @@ gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, c
 /* Bytes of device workspace gauss_sum_fwd_bwd needs (0 if p is invalid). */
 size_t gauss_sum_fwd_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv);
 
+/* A batch of `count` independent problems of one shape p (the paper's
+ * benchmark evaluates B point clouds at once, Sec. 4).  Problem b reads
+ * q + b*q_stride, k + b*k_stride, v + b*v_stride, dout + b*dout_stride and
+ * writes out + b*out_stride, dq + b*dq_stride, dk + b*dk_stride,
+ * dv + b*dv_stride; strides count elements of each array's own dtype.  Input
+ * strides may be 0 (all problems share that array, e.g. one key set); output
+ * strides must be at least one problem's output size when count > 1.  Every
+ * stride keeps the alignment rules of the single-problem call. */
+typedef struct {
+  int64_t count;
+  int64_t q_stride, k_stride, v_stride, dout_stride;
+  int64_t out_stride, dq_stride, dk_stride, dv_stride;
+} gs_batch;
+
+/* gauss_sum_fwd for each problem of the batch.  All validation (shapes,
+ * strides, alignment, overlaps of any output with any input, the workspace or
+ * another output) happens before anything is enqueued.  The problems run one
+ * after another on `stream` and share the workspace, whose size is
+ * gauss_sum_fwd_workspace_size(p); results equal the single-problem calls bit
+ * for bit.  count == 0 is a no-op (no pointer is used). */
+gs_status gauss_sum_fwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
+                                const void* k, const void* v, float tau, float* out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* gauss_sum_bwd for each problem of the batch (as gauss_sum_fwd_batched; the
+ * workspace size is gauss_sum_bwd_workspace_size(p, ...)). */
+gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
+                                const void* k, const void* v, float tau, const void* dout,
+                                gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* One MMD-flow evaluation (Sec. 3, the MMD and particle-flow paragraphs):
  * points x (N x D, qk_dtype) serve as both queries and keys, v (N x 1,
  * v_dtype) are the signed weights of sigma = mu - nu = sum_n v_n delta_{x_n}.

@@ -720,7 +720,8 @@ size_t workspace_for(const gs_problem* p, bool fwd, int want_dq, int want_dk, in
 // forward sum, dq / dk / dv: gradients; NULL = not requested).
 gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
               const void* dout, gs_dtype dout_dtype, float* out, float* dq, float* dk, float* dv,
-              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+              void* workspace, size_t workspace_bytes, hipStream_t stream,
+              bool validate_only = false) {
   gs_status st = check_problem(p);
   if (st != GS_SUCCESS) return st;
   if ((st = check_tau(tau)) != GS_SUCCESS) return st;
@@ -745,6 +746,7 @@ gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, 
       if (overlap(outs[a], outs[b])) return GS_ERR_ALIAS;
   }
   if (M == 0 || N == 0) {
+    if (validate_only) return GS_SUCCESS;
     // Empty sums: every requested output is zero.
     if (M > 0) {
       fill_zero(stream, out, M * C);
@@ -771,6 +773,7 @@ gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, 
   Range rw = range_of(workspace, (int64_t)pl.total);
   for (int a = 0; a < 4; ++a)
     if (overlap(outs[a], rw) || overlap(in[a], rw)) return GS_ERR_ALIAS;
+  if (validate_only) return GS_SUCCESS;
   make_plan(*p, w, alias, workspace, pl);
 
   Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
@@ -806,6 +809,65 @@ gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, 
             pl.slots + 0, v, p->v_dtype, dk);
   if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv);
   return launch_status();
+}
+
+
+// A batch of problems of one shape: every problem is validated first (its
+// pointers, and the spans of all outputs against the spans of all inputs,
+// the workspace and each other), then each runs through run() in order.
+gs_status run_batched(const gs_problem* p, const gs_batch* b, const void* q, const void* k,
+                      const void* v, float tau, const void* dout, gs_dtype dout_dtype, float* out,
+                      float* dq, float* dk, float* dv, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream) {
+  gs_status st = check_problem(p);
+  if (st != GS_SUCCESS) return st;
+  if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+  if (!b) return GS_ERR_NULL_POINTER;
+  const int64_t cnt = b->count, M = p->M, N = p->N, D = p->D, C = p->C;
+  if (cnt < 0 || b->q_stride < 0 || b->k_stride < 0 || b->v_stride < 0 || b->dout_stride < 0 ||
+      b->out_stride < 0 || b->dq_stride < 0 || b->dk_stride < 0 || b->dv_stride < 0)
+    return GS_ERR_BAD_SHAPE;
+  if (cnt == 0) return GS_SUCCESS;  // nothing to compute, no pointer is used
+  const bool grads = dq || dk || dv;
+  if (!out && !grads) return GS_ERR_NULL_POINTER;
+  if (grads && !valid_dtype(dout_dtype)) return GS_ERR_UNSUPPORTED;
+  const int64_t vs = (int64_t)dsize(p->v_dtype), gsz = (int64_t)dsize(dout_dtype);
+  if (cnt > 1 && ((out && b->out_stride < M * C) || (dq && b->dq_stride < M * D) ||
+                  (dk && b->dk_stride < N * D) || (dv && b->dv_stride < N * C)))
+    return GS_ERR_BAD_SHAPE;
+  // (strides count elements, so every problem's pointers keep the alignment
+  // of the first one's; the per-problem validation below checks it)
+  // spans over the whole batch
+  auto span = [&](const void* base, int64_t stride, int64_t esize, int64_t elems) {
+    return range_of(base, base ? ((cnt - 1) * stride + elems) * esize : 0);
+  };
+  const Range in[4] = {span(q, b->q_stride, 2, M * D), span(k, b->k_stride, 2, N * D),
+                       span(v, b->v_stride, vs, N * C),
+                       span(grads ? dout : nullptr, b->dout_stride, gsz, M * C)};
+  const Range outs[4] = {span(out, b->out_stride, 4, M * C), span(dq, b->dq_stride, 4, M * D),
+                         span(dk, b->dk_stride, 4, N * D), span(dv, b->dv_stride, 4, N * C)};
+  for (int a = 0; a < 4; ++a) {
+    for (int c = 0; c < 4; ++c)
+      if (overlap(outs[a], in[c])) return GS_ERR_ALIAS;
+    for (int c = a + 1; c < 4; ++c)
+      if (overlap(outs[a], outs[c])) return GS_ERR_ALIAS;
+  }
+  auto at = [](const void* base, int64_t i, int64_t stride, int64_t esize) -> const char* {
+    return base ? static_cast<const char*>(base) + i * stride * esize : nullptr;
+  };
+  auto at_w = [](float* base, int64_t i, int64_t stride) -> float* {
+    return base ? base + i * stride : nullptr;
+  };
+  for (int pass = 0; pass < 2; ++pass) {  // 0: validate every problem, 1: run them
+    for (int64_t i = 0; i < cnt; ++i) {
+      st = run(p, at(q, i, b->q_stride, 2), at(k, i, b->k_stride, 2), at(v, i, b->v_stride, vs), tau,
+               at(dout, i, b->dout_stride, gsz), dout_dtype, at_w(out, i, b->out_stride),
+               at_w(dq, i, b->dq_stride), at_w(dk, i, b->dk_stride), at_w(dv, i, b->dv_stride),
+               workspace, workspace_bytes, stream, pass == 0);
+      if (st != GS_SUCCESS) return st;
+    }
+  }
+  return GS_SUCCESS;
 }
 
 }  // namespace
@@ -929,4 +991,27 @@ gs_status gauss_sum_mmd_flow(const gs_problem* p, const void* x, const void* v, 
     return GS_ERR_INTERNAL;
   }
 }
+gs_status gauss_sum_fwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
+                                const void* k, const void* v, float tau, float* out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  try {
+    return run_batched(p, batch, q, k, v, tau, nullptr, GS_F32, out, nullptr, nullptr, nullptr,
+                       workspace, workspace_bytes, stream);
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
+
+gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
+                                const void* k, const void* v, float tau, const void* dout,
+                                gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  try {
+    return run_batched(p, batch, q, k, v, tau, dout, dout_dtype, nullptr, dq, dk, dv, workspace,
+                       workspace_bytes, stream);
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
+
 }  // extern "C"

@@ -30,7 +30,8 @@ STATUS = {
 EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_bwd", "gauss_sum_fwd_workspace_size",
             "gauss_sum_bwd_workspace_size", "gauss_sum_fwd_bwd_workspace_size",
             "gauss_sum_status_string", "gauss_sum_abi_version", "gauss_sum_profile_start",
-            "gauss_sum_profile_stop", "gauss_sum_mmd_flow", "gauss_sum_mmd_flow_workspace_size")
+            "gauss_sum_profile_stop", "gauss_sum_mmd_flow", "gauss_sum_mmd_flow_workspace_size",
+            "gauss_sum_fwd_batched", "gauss_sum_bwd_batched")
 PROFILE_FWD, PROFILE_GRAD = 1, 2
 
 
@@ -39,6 +40,13 @@ class GaussSumError(RuntimeError):
         self.status = status
         msg = "%s failed: %s (%s)" % (where, STATUS.get(status, "?"), status_string(status))
         super().__init__(msg)
+
+
+class Batch(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int64), ("q_stride", ctypes.c_int64), ("k_stride", ctypes.c_int64),
+                ("v_stride", ctypes.c_int64), ("dout_stride", ctypes.c_int64),
+                ("out_stride", ctypes.c_int64), ("dq_stride", ctypes.c_int64),
+                ("dk_stride", ctypes.c_int64), ("dv_stride", ctypes.c_int64)]
 
 
 class Problem(ctypes.Structure):
@@ -73,6 +81,12 @@ def load(path=LIB_PATH):
     lib.gauss_sum_fwd_bwd.restype = ctypes.c_int
     lib.gauss_sum_fwd_bwd_workspace_size.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int]
     lib.gauss_sum_fwd_bwd_workspace_size.restype = sz
+    BP = ctypes.POINTER(Batch)
+    lib.gauss_sum_fwd_batched.argtypes = [P, BP, vp, vp, vp, ctypes.c_float, f32p, vp, sz, vp]
+    lib.gauss_sum_fwd_batched.restype = ctypes.c_int
+    lib.gauss_sum_bwd_batched.argtypes = [P, BP, vp, vp, vp, ctypes.c_float, vp, ctypes.c_int, f32p,
+                                          f32p, f32p, vp, sz, vp]
+    lib.gauss_sum_bwd_batched.restype = ctypes.c_int
     lib.gauss_sum_mmd_flow.argtypes = [P, vp, vp, ctypes.c_float, f32p, f32p, vp, vp, sz, vp]
     lib.gauss_sum_mmd_flow.restype = ctypes.c_int
     lib.gauss_sum_mmd_flow_workspace_size.argtypes = [P]
@@ -254,6 +268,79 @@ def gauss_sum_fwd_bwd(q, k, v, tau, dout, want=(True, True, True), out=None, wor
     if st != 0:
         raise GaussSumError(st, "gauss_sum_fwd_bwd")
     return out, dq, dk, dv
+
+
+def _batched_inputs(q, k, v):
+    """(B, M, N, D, C, strides) for q: B x M x D, k: B x N x D or N x D (shared),
+    v: B x N x C or N x C (shared); contiguous GPU tensors."""
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous GPU tensor" % name)
+    if q.dim() != 3:
+        raise ValueError("q must be B x M x D")
+    B, M, D = q.shape
+    if k.dim() not in (2, 3) or v.dim() not in (2, 3) or k.shape[-1] != D:
+        raise ValueError("k must be [B x] N x D and v [B x] N x C")
+    N, C = v.shape[-2], v.shape[-1]
+    if k.shape[-2] != N or (k.dim() == 3 and k.shape[0] != B) or (v.dim() == 3 and v.shape[0] != B):
+        raise ValueError("inconsistent batch shapes")
+    if q.dtype != k.dtype:
+        raise TypeError("q and k must share a dtype")
+    ks = N * D if k.dim() == 3 else 0
+    vs = N * C if v.dim() == 3 else 0
+    return B, M, N, D, C, M * D, ks, vs
+
+
+def gauss_sum_fwd_batched(q, k, v, tau, out=None, workspace=None, stream=None):
+    """B independent forward sums: q is B x M x D, k and v are B x N x (D, C)
+    or shared N x (D, C); returns B x M x C fp32."""
+    import torch
+    B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
+    p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
+    lib = load()
+    if out is None:
+        out = torch.empty((B, M, C), dtype=torch.float32, device=q.device)
+    b = Batch(B, qs, ks, vs, 0, M * C, 0, 0, 0)
+    need = int(lib.gauss_sum_fwd_workspace_size(ctypes.byref(p)))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, q.device)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_fwd_batched(ctypes.byref(p), ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v),
+                                   float(tau), _ptr(out), _ptr(workspace), wbytes, _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_fwd_batched")
+    return out
+
+
+def gauss_sum_bwd_batched(q, k, v, tau, dout, want=(True, True, True), workspace=None, stream=None):
+    """Gradients of B independent problems (q, k shared as in
+    gauss_sum_fwd_batched; dout is B x M x C); each output B x (rows) x (D or C)."""
+    import torch
+    B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
+    if not dout.is_cuda or dout.shape != (B, M, C) or not dout.is_contiguous():
+        raise ValueError("dout must be a contiguous %d x %d x %d GPU tensor" % (B, M, C))
+    if (want[1] and ks == 0) or (want[2] and vs == 0):
+        raise ValueError("dk / dv of a shared key set: sum the per-problem gradients instead")
+    p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
+    lib = load()
+    dev = q.device
+    dq = torch.empty((B, M, D), dtype=torch.float32, device=dev) if want[0] else None
+    dk = torch.empty((B, N, D), dtype=torch.float32, device=dev) if want[1] else None
+    dv = torch.empty((B, N, C), dtype=torch.float32, device=dev) if want[2] else None
+    b = Batch(B, qs, ks, vs, M * C, 0, M * D, N * D, N * C)
+    need = int(lib.gauss_sum_bwd_workspace_size(ctypes.byref(p), int(bool(want[0])),
+                                                int(bool(want[1])), int(bool(want[2]))))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, dev)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_bwd_batched(ctypes.byref(p), ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v),
+                                   float(tau), _ptr(dout), _dtype_code(dout.dtype), _ptr(dq), _ptr(dk),
+                                   _ptr(dv), _ptr(workspace), wbytes, _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_bwd_batched")
+    return dq, dk, dv
 
 
 def gauss_sum_mmd_flow_workspace_size(N, D, qk_dtype=GS_F16, v_dtype=GS_F32):

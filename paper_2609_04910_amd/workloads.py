@@ -193,6 +193,34 @@ def make(name: str, seed: int = 0, M: Optional[int] = None, N: Optional[int] = N
     raise KeyError(name)
 
 
+BATCHED = {
+    # Sec. 4 benchmark layout: B independent standard Gaussian clouds scaled by
+    # D^(-1/2), M = N, tau = 1, fp16 (the D sweep uses B = 64, N = 16384, C = 1)
+    "batch_d32": dict(B=64, M=16384, N=16384, D=32, C=1),
+}
+
+
+def make_batch(name: str, seed: int = 0, B: Optional[int] = None, M: Optional[int] = None):
+    """Batched workload ``name``: (q, k, v, tau) with q, k of shape B x M x D
+    (fp16, N(0, I / D)) and v of shape B x N x C (fp32, N(0, 1)); draws in the
+    order points (q then k, problem by problem), then values."""
+    cfg = dict(BATCHED[name])
+    if B is not None:
+        cfg["B"] = B
+    if M is not None:
+        cfg["M"] = cfg["N"] = M
+    B_, M_, N_, D_, C_ = cfg["B"], cfg["M"], cfg["N"], cfg["D"], cfg["C"]
+    rng = np.random.default_rng(seed)
+    s = np.float32(1.0 / np.sqrt(D_))
+    q = np.empty((B_, M_, D_), np.float16)
+    k = np.empty((B_, N_, D_), np.float16)
+    for b in range(B_):
+        q[b] = (rng.standard_normal((M_, D_), dtype=np.float32) * s).astype(np.float16)
+        k[b] = (rng.standard_normal((N_, D_), dtype=np.float32) * s).astype(np.float16)
+    v = rng.standard_normal((B_, N_, C_), dtype=np.float32)
+    return q, k, v, np.float32(1.0)
+
+
 def sample_rows(n_total: int, count: int, seed: int = 1, tile: int = 256) -> np.ndarray:
     """Seeded sample of ``count`` distinct row indices plus tile-boundary rows
     (0, 63, 64, 127, 128, 255 modulo ``tile`` near the start and end) and the

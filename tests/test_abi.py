@@ -129,6 +129,46 @@ def test_mmd_flow_validation(kw, status):
     assert _flow(**kw) == status
 
 
+def _fwd_b(count=3, qs=8 * 4, ks=8 * 4, vs=8 * 2, outs=8 * 2, M=8, N=8, D=4, C=2, q=FAKE,
+           k=FAKE + 0x10000, v=FAKE + 0x20000, out=FAKE + 0x30000, ws=FAKE + 0x100000, wsb=1 << 40,
+           batch=True):
+    lib = gs.load()
+    prob = gs.make_problem(M, N, D, C, gs.GS_F16, gs.GS_F32)
+    b = gs.Batch(count, qs, ks, vs, 0, outs, 0, 0, 0)
+    bp = ctypes.byref(b) if batch else None
+    return lib.gauss_sum_fwd_batched(ctypes.byref(prob), bp, q, k, v, ctypes.c_float(1.0), out, ws,
+                                     wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=False), 1), (dict(out=None), 1), (dict(count=-1), 2), (dict(qs=-8), 2),
+    (dict(outs=15), 2), (dict(count=0), 0), (dict(count=0, out=None), 0), (dict(q=FAKE + 1), 5),
+    (dict(out=FAKE + 0x20000 + 2 * 8 * 2 * 4), 9),  # third problem's out meets the v span
+    (dict(outs=16, out=FAKE + 0x100000 - 64), 9),    # out span runs into the workspace
+    (dict(wsb=16), 6), (dict(D=0), 2),
+])
+def test_fwd_batched_validation(kw, status):
+    assert _fwd_b(**kw) == status
+
+
+def test_bwd_batched_validation():
+    lib = gs.load()
+    prob = gs.make_problem(8, 8, 4, 2, gs.GS_F16, gs.GS_F32)
+    b = gs.Batch(2, 32, 32, 16, 16, 0, 32, 32, 16)
+    args = [FAKE, FAKE + 0x10000, FAKE + 0x20000, ctypes.c_float(1.0), FAKE + 0x70000, gs.GS_F32]
+    ws = [FAKE + 0x100000, 1 << 40, None]
+    assert lib.gauss_sum_bwd_batched(ctypes.byref(prob), ctypes.byref(b), *args, None, None, None,
+                                     *ws) == 1
+    empty = gs.Batch(0, 32, 32, 16, 16, 0, 32, 32, 16)
+    assert lib.gauss_sum_bwd_batched(ctypes.byref(prob), ctypes.byref(empty), *args, None, None,
+                                     None, *ws) == 0
+    bad = gs.Batch(2, 32, 32, 16, 16, 0, 31, 32, 16)  # dq of problem 1 would overlap problem 0
+    assert lib.gauss_sum_bwd_batched(ctypes.byref(prob), ctypes.byref(bad), *args, FAKE + 0x40000,
+                                     None, None, *ws) == 2
+    assert lib.gauss_sum_bwd_batched(ctypes.byref(prob), ctypes.byref(b), *args, FAKE + 0x40000,
+                                     FAKE + 0x40000 + 64, None, *ws) == 9
+
+
 def test_empty_query_set_is_a_noop():
     # M = 0: nothing to compute; no pointer is touched and no kernel runs.
     assert _fwd(M=0, q=None, out=None) == 0
@@ -174,3 +214,4 @@ def test_no_device_reports_hip_error():
     assert _bwd() == 7
     assert _fb() == 7
     assert _flow() == 7
+    assert _fwd_b() == 7
