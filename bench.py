@@ -223,7 +223,8 @@ def bench_batched(args):
     B, M, D = q.shape
     N, C = v.shape[1], v.shape[2]
     tq, tk, tv = (torch.from_numpy(a).to(dev) for a in (q, k, v))
-    p_ws = gs.gauss_sum_fwd_workspace_size(M, N, D, C, gs.GS_F16, gs.GS_F32)
+    # room for every problem in one launch group
+    p_ws = gs.gauss_sum_fwd_batched_workspace_size(M, N, D, C, B, gs.GS_F16, gs.GS_F32)
     ws = torch.empty(max(p_ws, 1), dtype=torch.uint8, device=dev)
     out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
@@ -252,7 +253,8 @@ def bench_batched(args):
     kernel_ms = gs.gauss_sum_profile_stop(cap)
     ms_per_step = e0.elapsed_time(e1) / args.steps
     pairs = float(B) * M * N
-    per_launch = float(M) * N * (2 * D + 2 * C)
+    per_step = max(1, len(kernel_ms) // args.steps)     # forward launches per step
+    per_launch = float(B) / per_step * M * N * (2 * D + 2 * C)
     avg = float(np.mean(kernel_ms)) if kernel_ms else float("nan")
     achieved = per_launch / (avg * 1e-3) / 1e12
     res = {
@@ -269,25 +271,24 @@ def bench_batched(args):
                      "peak": PEAK_MFMA_F16 / 1e12, "unit": "TFLOP/s",
                      "frac": achieved / (PEAK_MFMA_F16 / 1e12),
                      "traffic": recorded_traffic(args.workload, "k_fwd"), "avg_launch_ms": avg,
-                     "launches": len(kernel_ms), "flops_per_launch": per_launch,
-                     "launch_share_of_step": avg * B / ms_per_step},
+                     "launches": len(kernel_ms), "problems_per_launch": B // per_step,
+                     "flops_per_launch": per_launch,
+                     "launch_share_of_step": avg * per_step / ms_per_step},
     }
     if not args.no_cpu:
         threads = min(oracle.default_threads(), 16)
         oracle.fwd(q[0], k[0], v[0], float(tau), rows=np.arange(1), threads=threads)
-        rows = np.arange(64)
-        t = time.perf_counter()
-        oracle.fwd(q[0], k[0], v[0], float(tau), rows=rows, threads=threads)
-        t = time.perf_counter() - t
-        n_rows = int(min(M, max(64, 64 * args.cpu_budget / max(t, 1e-3))))
-        rows = np.sort(np.random.default_rng(3).choice(M, size=n_rows, replace=False))
-        t = time.perf_counter()
-        oracle.fwd(q[0], k[0], v[0], float(tau), rows=rows, threads=threads)
-        t = time.perf_counter() - t
-        res["cpu_baseline"] = {"value": n_rows * N / t, "unit": "pairs/s", "cores": threads,
+        # whole problems (every query row against every key), in order, until
+        # the time budget is spent
+        t0, done = time.perf_counter(), 0
+        while done < B and (done == 0 or time.perf_counter() - t0 < args.cpu_budget):
+            oracle.fwd(q[done], k[done], v[done], float(tau), threads=threads)
+            done += 1
+        t = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": done * float(M) * N / t, "unit": "pairs/s", "cores": threads,
                                "kind": "oracle",
-                               "sample": "fp64 oracle, forward on %d of %d query rows of problem 0, "
-                                         "each against all %d keys, %.1f s" % (n_rows, M, N, t)}
+                               "sample": "fp64 oracle, forward of problems 0..%d of %d (all %d x %d "
+                                         "pairs each), %.1f s" % (done - 1, B, M, N, t)}
     print(json.dumps(res), flush=True)
 
 

@@ -140,20 +140,39 @@ typedef struct {
 
 /* gauss_sum_fwd for each problem of the batch.  All validation (shapes,
  * strides, alignment, overlaps of any output with any input, the workspace or
- * another output) happens before anything is enqueued.  The problems run one
- * after another on `stream` and share the workspace, whose size is
- * gauss_sum_fwd_workspace_size(p); results equal the single-problem calls bit
- * for bit.  count == 0 is a no-op (no pointer is used). */
+ * another output) happens before anything is enqueued; count == 0 is a no-op
+ * (no pointer is used).
+ *
+ * The problems run in launch groups on `stream`: every kernel launch covers
+ * a whole group (one grid dimension indexes the problem), each problem of the
+ * group using its own slice of the workspace.  The workspace must hold at
+ * least one slice, gauss_sum_fwd_workspace_size(p) bytes (then the problems
+ * run one at a time); gauss_sum_fwd_batched_workspace_size(p, count) bytes
+ * let all of them (up to 65535) share each launch, and any size in between
+ * gives groups of as many problems as fit.  Group sizes change how the key
+ * range of a problem is split (and so the fp32 summation order): results are
+ * reproducible bit for bit for equal arguments, and within the tolerance of
+ * the single-problem call otherwise. */
 gs_status gauss_sum_fwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
                                 const void* k, const void* v, float tau, float* out,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* gauss_sum_bwd for each problem of the batch (as gauss_sum_fwd_batched; the
- * workspace size is gauss_sum_bwd_workspace_size(p, ...)). */
+/* Workspace bytes for gauss_sum_fwd_batched to run `count` problems of shape
+ * p in one launch group (count capped at 65535); 0 if p is invalid, empty or
+ * count < 1. */
+size_t gauss_sum_fwd_batched_workspace_size(const gs_problem* p, int64_t count);
+
+/* gauss_sum_bwd for each problem of the batch (as gauss_sum_fwd_batched; one
+ * slice is gauss_sum_bwd_workspace_size(p, ...) bytes). */
 gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
                                 const void* k, const void* v, float tau, const void* dout,
                                 gs_dtype dout_dtype, float* dq, float* dk, float* dv,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes for gauss_sum_bwd_batched to run `count` problems in one
+ * launch group (as gauss_sum_fwd_batched_workspace_size). */
+size_t gauss_sum_bwd_batched_workspace_size(const gs_problem* p, int64_t count, int want_dq,
+                                            int want_dk, int want_dv);
 
 /* One MMD-flow evaluation (Sec. 3, the MMD and particle-flow paragraphs):
  * points x (N x D, qk_dtype) serve as both queries and keys, v (N x 1,

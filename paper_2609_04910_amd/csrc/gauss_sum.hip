@@ -74,15 +74,20 @@ constexpr int dq_qt(int DP, int CW) {
 
 using FwdFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
                        const uint4*, const float*, const uint4*, const uint32_t*, float, int64_t, int,
-                       int, int, float*, int64_t);
+                       int, int, float*, int64_t, const Bz&);
 
+// grid.z > 1: the batched instance (problem blockIdx.z at the strides of bz).
 template <typename T, int DP, int CT, bool ONE>
 void launch_fwd(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const uint4* srt,
                 const float* snh, const uint4* ks, const float* scal, const uint4* vt,
                 const uint32_t* vslot, float tau2, int64_t M, int C, int steps, int sps, float* out,
-                int64_t pstride) {
-  hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE>), grid, dim3(kBlockThreads), 0, st, qs,
-                     nhq, srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride);
+                int64_t pstride, const Bz& bz) {
+  if (grid.z > 1)
+    hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, true>), grid, dim3(kBlockThreads), 0, st,
+                       qs, nhq, srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride, bz);
+  else
+    hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, false>), grid, dim3(kBlockThreads), 0, st,
+                       qs, nhq, srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride, bz);
 }
 
 // A launcher and the kernel it launches (for occupancy queries).
@@ -94,7 +99,7 @@ struct FwdK {
 template <typename T, int DP, int CT, bool ONE>
 FwdK fwd_k() {
   return {&launch_fwd<T, DP, CT, ONE>,
-          reinterpret_cast<const void*>(&k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE>)};
+          reinterpret_cast<const void*>(&k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, false>)};
 }
 
 // CT = 0 selects the single-channel form (one 16-row tile of signs).
@@ -125,7 +130,8 @@ FwdK fwd_fn(int DP, int CT) {
 using DqFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
                       const uint4*, const float*, const uint4*, const uint32_t*, const uint4*,
                       const uint32_t*, const uint4*, const uint32_t*, const void*, int, float, float,
-                      int64_t, int, int, int, float*, int64_t, const uint4*, int, float*, int64_t);
+                      int64_t, int, int, int, float*, int64_t, const uint4*, int, float*, int64_t,
+                      const Bz&);
 
 template <typename T, int DP, int CW, int FCT>
 void launch_dq(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, const uint4* srt,
@@ -133,10 +139,15 @@ void launch_dq(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, con
                const uint32_t* kslot, const uint4* vs, const uint32_t* vslot, const uint4* gsr,
                const uint32_t* gslot, const void* g1, int g1_dtype, float tau2, float tau, int64_t M,
                int D, int steps, int sps, float* out, int64_t pstride, const uint4* vt, int C,
-               float* out_s, int64_t pstride_s) {
-  hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT>), grid, dim3(kBlockThreads), 0, st, qs, nhq,
-                     srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, g1, g1_dtype, tau2, tau, M,
-                     D, steps, sps, out, pstride, vt, C, out_s, pstride_s);
+               float* out_s, int64_t pstride_s, const Bz& bz) {
+  if (grid.z > 1)
+    hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT, true>), grid, dim3(kBlockThreads), 0, st, qs,
+                       nhq, srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, g1, g1_dtype, tau2, tau,
+                       M, D, steps, sps, out, pstride, vt, C, out_s, pstride_s, bz);
+  else
+    hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT, false>), grid, dim3(kBlockThreads), 0, st, qs,
+                       nhq, srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, g1, g1_dtype, tau2, tau,
+                       M, D, steps, sps, out, pstride, vt, C, out_s, pstride_s, bz);
 }
 
 struct DqK {
@@ -147,7 +158,7 @@ struct DqK {
 template <typename T, int DP, int CW, int FCT>
 DqK dq_k() {
   return {&launch_dq<T, DP, CW, FCT>,
-          reinterpret_cast<const void*>(&k_dq<T, DP, CW, dq_qt(DP, CW), FCT>)};
+          reinterpret_cast<const void*>(&k_dq<T, DP, CW, dq_qt(DP, CW), FCT, false>)};
 }
 
 // fused: also produce the forward sum (one 16-row tile: C = 1 through the
@@ -208,8 +219,11 @@ struct Vals {  // one value set (v or dout)
   uint16_t* ks = nullptr;
 };
 
+// One problem's slice of the workspace (a batch puts G slices back to back,
+// problem z at z * total bytes).
 struct Plan {
   Dims dm;
+  int64_t G = 1;               // problems sharing each launch (split counts are chosen for G)
   int64_t Mp = 0, Np = 0;
   bool alias = false;          // q and k are the same array
   uint32_t* slots = nullptr;   // [0] |v| max, [1] |dout| max, [2] |q| max, [3] |k| max
@@ -257,16 +271,18 @@ int device_slots(const void* kernel) {
 // parts (partial sums combined afterwards): the split count that minimises
 // (rounds of resident workgroups) x (steps per split + fixed cost), searched
 // from the smallest count that fills the device once up to four times that.
-PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel) {
+// `group` problems run side by side on grid.z.
+PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel, int64_t group) {
   PassShape ps;
   ps.blocks = (int)ceil_div(rows, 64 * QT);
   ps.steps = (int)ceil_div(keys, kStep);
   const int64_t slots = device_slots(kernel);
+  const int64_t wide = (int64_t)std::max(1, ps.blocks) * std::max<int64_t>(1, group);
   const int cap = std::max(1, ps.steps / kMinStepsPerSplit);
-  const int lo = (int)std::min<int64_t>(cap, std::max<int64_t>(1, ceil_div(slots, std::max(1, ps.blocks))));
+  const int lo = (int)std::min<int64_t>(cap, std::max<int64_t>(1, ceil_div(slots, wide)));
   const int hi = std::min(cap, 4 * lo);
   auto cost = [&](int sp) {
-    return ceil_div((int64_t)ps.blocks * sp, slots) * (ceil_div(ps.steps, sp) + kSplitOverheadSteps);
+    return ceil_div(wide * sp, slots) * (ceil_div(ps.steps, sp) + kSplitOverheadSteps);
   };
   int splits = lo;
   int64_t best = cost(lo);
@@ -319,10 +335,11 @@ DqK dq_for(const gs_problem& p, const Dims& dm, bool fused) {
 const void* fwd_kernel(const gs_problem& p, const Dims& dm) { return fwd_for(p, dm).kernel; }
 const void* dq_kernel(const gs_problem& p, const Dims& dm, bool fused) { return dq_for(p, dm, fused).kernel; }
 
-// Lays out every buffer the requested passes need; with ws == nullptr only
-// computes the size.
-void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& pl) {
+// Lays out every buffer the requested passes need for one problem of a group
+// of G; with ws == nullptr only computes the size.
+void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& pl, int64_t G) {
   pl.dm = dims_of(p.D, p.C);
+  pl.G = G;
   pl.Mp = round_up(std::max<int64_t>(p.M, 1), kRowPad);
   pl.Np = round_up(std::max<int64_t>(p.N, 1), kRowPad);
   pl.alias = alias;
@@ -367,7 +384,7 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   // Partial-sum buffer for split passes (reused by every pass in turn).
   size_t part = 0, part_s = 0;
   auto consider = [&](int64_t rows, int64_t keys, int QT, int64_t width, const void* kernel) {
-    PassShape ps = pass_shape(rows, keys, QT, kernel);
+    PassShape ps = pass_shape(rows, keys, QT, kernel, G);
     if (ps.splits > 1) part = std::max(part, (size_t)ps.splits * rows * width * 4);
     return ps.splits;
   };
@@ -422,84 +439,106 @@ inline unsigned grid1(int64_t n, int threads = 256) {
 // Reductions: at most 512 workgroups (grid-stride), one atomic each.
 inline unsigned grid_reduce(int64_t n) { return std::min(grid1(n), 512u); }
 
+// A launch group: G problems on grid.z, each with a workspace slice of
+// `slice` bytes (pl describes the first one).
 struct Ctx {
   hipStream_t st;
   const gs_problem* p;
   Plan* pl;
   float tau, tau2;
+  unsigned G;
+  int64_t slice;
 };
 
-// sgn / sgn_dt: for single-channel problems, the values whose signs the KS
-// copy of these points (as keys of a gradient pass) carries; else NULL.
+inline Bz bz_ws(const Ctx& c) {
+  Bz b;
+  b.ws = c.slice;
+  return b;
+}
+inline dim3 grid_g(const Ctx& c, unsigned x, unsigned y = 1) { return dim3(x, y, c.G); }
+
+// xs: byte stride of x between problems.  sgn / sgn_dt / sgns: for
+// single-channel problems, the values whose signs the KS copy of these points
+// (as keys of a gradient pass) carries, and their stride; else NULL.
 template <typename T>
-void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t n, int64_t n_pad, Side& s,
-                   uint32_t* slot, const void* sgn, gs_dtype sgn_dt) {
+void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t xs, int64_t n, int64_t n_pad, Side& s,
+                   uint32_t* slot, const void* sgn, gs_dtype sgn_dt, int64_t sgns) {
   const gs_problem& p = *c.p;
   const int W = c.pl->dm.W();
-  hipLaunchKernelGGL(k_points_rt_norm<T>, dim3(grid1(n_pad * (W / 8))), dim3(256), 0, c.st, x16, n,
-                     (int)p.D, n_pad, W, s.rt, s.nh);
+  Bz bz = bz_ws(c);
+  bz.in = xs;
+  bz.in2 = sgns;
+  hipLaunchKernelGGL(k_points_rt_norm<T>, grid_g(c, grid1(n_pad * (W / 8))), dim3(256), 0, c.st, x16, n,
+                     (int)p.D, n_pad, W, s.rt, s.nh, bz);
   if (s.samp_rt)
-    hipLaunchKernelGGL(k_sample, dim3(grid1(kSampleRows * W)), dim3(256), 0, c.st, x16, n, (int)p.D, W,
-                       (const float*)s.nh, s.samp_rt, s.samp_nh);
+    hipLaunchKernelGGL(k_sample, grid_g(c, grid1(kSampleRows * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
+                       W, (const float*)s.nh, s.samp_rt, s.samp_nh, bz);
   if (s.ks) {
     const uint32_t* sl = nullptr;
     if (p.qk_dtype == GS_BF16) {
-      hipLaunchKernelGGL(k_absmax, dim3(grid_reduce(n * p.D)), dim3(256), 0, c.st,
-                         static_cast<const void*>(x16), n * p.D, 2, slot);
+      hipLaunchKernelGGL(k_absmax, grid_g(c, grid_reduce(n * p.D)), dim3(256), 0, c.st,
+                         static_cast<const void*>(x16), n * p.D, 2, slot, bz);
       sl = slot;
     }
-    hipLaunchKernelGGL(k_points_ks<T>, dim3(grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
-                       n_pad, W, sl, sgn, (int)sgn_dt, s.ks);
+    hipLaunchKernelGGL(k_points_ks<T>, grid_g(c, grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n,
+                       (int)p.D, n_pad, W, sl, sgn, (int)sgn_dt, s.ks, bz);
   }
 }
 
-void prep_points(const Ctx& c, const void* x, int64_t n, int64_t n_pad, Side& s, uint32_t* slot,
-                 const void* sgn = nullptr, gs_dtype sgn_dt = GS_F32) {
+void prep_points(const Ctx& c, const void* x, int64_t xs, int64_t n, int64_t n_pad, Side& s,
+                 uint32_t* slot, const void* sgn = nullptr, gs_dtype sgn_dt = GS_F32, int64_t sgns = 0) {
   const uint16_t* x16 = static_cast<const uint16_t*>(x);
   if (c.p->qk_dtype == GS_F16)
-    prep_points_t<F16>(c, x16, n, n_pad, s, slot, sgn, sgn_dt);
+    prep_points_t<F16>(c, x16, xs, n, n_pad, s, slot, sgn, sgn_dt, sgns);
   else
-    prep_points_t<BF16>(c, x16, n, n_pad, s, slot, sgn, sgn_dt);
+    prep_points_t<BF16>(c, x16, xs, n, n_pad, s, slot, sgn, sgn_dt, sgns);
 }
 
 // KS copy only (the second, differently signed copy of aliased points).
-void prep_points_ks(const Ctx& c, const void* x, int64_t n, int64_t n_pad, uint16_t* ks,
-                    uint32_t* slot, const void* sgn, gs_dtype sgn_dt) {
+void prep_points_ks(const Ctx& c, const void* x, int64_t xs, int64_t n, int64_t n_pad, uint16_t* ks,
+                    uint32_t* slot, const void* sgn, gs_dtype sgn_dt, int64_t sgns) {
   const gs_problem& p = *c.p;
   const int W = c.pl->dm.W();
   const uint16_t* x16 = static_cast<const uint16_t*>(x);
   const uint32_t* sl = p.qk_dtype == GS_BF16 ? slot : nullptr;
+  Bz bz = bz_ws(c);
+  bz.in = xs;
+  bz.in2 = sgns;
   if (p.qk_dtype == GS_F16)
-    hipLaunchKernelGGL(k_points_ks<F16>, dim3(grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
-                       n_pad, W, sl, sgn, (int)sgn_dt, ks);
+    hipLaunchKernelGGL(k_points_ks<F16>, grid_g(c, grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n,
+                       (int)p.D, n_pad, W, sl, sgn, (int)sgn_dt, ks, bz);
   else
-    hipLaunchKernelGGL(k_points_ks<BF16>, dim3(grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n,
-                       (int)p.D, n_pad, W, sl, sgn, (int)sgn_dt, ks);
+    hipLaunchKernelGGL(k_points_ks<BF16>, grid_g(c, grid1(n_pad / 8 * W)), dim3(256), 0, c.st, x16, n,
+                       (int)p.D, n_pad, W, sl, sgn, (int)sgn_dt, ks, bz);
 }
 
-void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t n, int64_t n_pad, Vals& s,
-                 uint32_t* slot) {
+void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t xs, int64_t n, int64_t n_pad,
+                 Vals& s, uint32_t* slot) {
   const gs_problem& p = *c.p;
   const int Wv = c.pl->dm.Wv(), Rv = c.pl->dm.Rv();
+  Bz bz = bz_ws(c);
+  bz.in = xs;
   if (n > 0)
-    hipLaunchKernelGGL(k_absmax, dim3(grid_reduce(n * p.C)), dim3(256), 0, c.st, x, n * p.C, (int)dt,
-                       slot);
+    hipLaunchKernelGGL(k_absmax, grid_g(c, grid_reduce(n * p.C)), dim3(256), 0, c.st, x, n * p.C, (int)dt,
+                       slot, bz);
   if (s.rt)
-    hipLaunchKernelGGL(k_values_rt, dim3(grid1(n_pad * Wv)), dim3(256), 0, c.st, x, (int)dt, n,
-                       (int)p.C, n_pad, Wv, (const uint32_t*)slot, s.rt);
+    hipLaunchKernelGGL(k_values_rt, grid_g(c, grid1(n_pad * Wv)), dim3(256), 0, c.st, x, (int)dt, n,
+                       (int)p.C, n_pad, Wv, (const uint32_t*)slot, s.rt, bz);
   if (s.ks)
-    hipLaunchKernelGGL(k_values_ks, dim3(grid1(n_pad * Rv)), dim3(256), 0, c.st, x, (int)dt, n,
-                       (int)p.C, n_pad, Rv, (const uint32_t*)slot, (int)(p.C == 1), s.ks);
+    hipLaunchKernelGGL(k_values_ks, grid_g(c, grid1(n_pad * Rv)), dim3(256), 0, c.st, x, (int)dt, n,
+                       (int)p.C, n_pad, Rv, (const uint32_t*)slot, (int)(p.C == 1), s.ks, bz);
 }
 
-// Per-step key scalars of key side `s` paired with values x (slot = their
-// absolute maximum): single-channel problems fold log2|v| and sign(v) in,
-// otherwise half norms only.
-void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64_t n, int64_t n_pad,
-                  const uint32_t* slot, float* out) {
+// Per-step key scalars of key side `s` paired with values x (byte stride xs,
+// slot = their absolute maximum): single-channel problems fold log2|v| and
+// sign(v) in, otherwise half norms only.
+void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64_t xs, int64_t n,
+                  int64_t n_pad, const uint32_t* slot, float* out) {
   const bool vals = c.p->C == 1 && x != nullptr;
-  hipLaunchKernelGGL(k_step_scalars, dim3(grid1(n_pad * 2)), dim3(256), 0, c.st, (const float*)s.nh,
-                     vals ? x : nullptr, (int)dt, n, n_pad, slot, c.tau2, out);
+  Bz bz = bz_ws(c);
+  bz.in = vals ? xs : 0;
+  hipLaunchKernelGGL(k_step_scalars, grid_g(c, grid1(n_pad * 2)), dim3(256), 0, c.st, (const float*)s.nh,
+                     vals ? x : nullptr, (int)dt, n, n_pad, slot, c.tau2, out, bz);
 }
 
 // Row-bound flags of the rows of `qs` (n rows, n_pad padded) against the
@@ -507,14 +546,15 @@ void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64
 template <typename T>
 void row_check_t(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Side& ks) {
   uint32_t* shift = reinterpret_cast<uint32_t*>(ks.samp_nh + kSampleRows);
-  const dim3 grid((unsigned)(n_pad / 256)), block(kBlockThreads);
+  const dim3 grid = grid_g(c, (unsigned)(n_pad / 256)), block(kBlockThreads);
   const uint4* q = (const uint4*)qs.rt;
   const uint4* s = (const uint4*)ks.samp_rt;
+  const Bz bz = bz_ws(c);
   switch (c.pl->dm.DP) {
-    case 1: hipLaunchKernelGGL((k_row_check<T, 1>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
-    case 2: hipLaunchKernelGGL((k_row_check<T, 2>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
-    case 4: hipLaunchKernelGGL((k_row_check<T, 4>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
-    case 8: hipLaunchKernelGGL((k_row_check<T, 8>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift); break;
+    case 1: hipLaunchKernelGGL((k_row_check<T, 1>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
+    case 2: hipLaunchKernelGGL((k_row_check<T, 2>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
+    case 4: hipLaunchKernelGGL((k_row_check<T, 4>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
+    case 8: hipLaunchKernelGGL((k_row_check<T, 8>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
   }
 }
 
@@ -525,58 +565,67 @@ void row_check(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Sid
     row_check_t<BF16>(c, qs, n, n_pad, ks);
 }
 
-void combine(const Ctx& c, const PassShape& ps, int64_t count, float* out) {
-  if (ps.splits > 1)
-    hipLaunchKernelGGL(k_combine, dim3(grid1(count)), dim3(256), 0, c.st, (const float*)c.pl->part,
-                       ps.splits, count, out);
+// Split partials (in the workspace slices) -> out (byte stride out_stride).
+void combine(const Ctx& c, const PassShape& ps, const float* part, int64_t count, float* out,
+             int64_t out_stride) {
+  if (ps.splits <= 1) return;
+  Bz bz = bz_ws(c);
+  bz.out = out_stride;
+  hipLaunchKernelGGL(k_combine, grid_g(c, grid1(count)), dim3(256), 0, c.st, part, ps.splits, count, out,
+                     bz);
 }
 
-// Forward-type pass: out[m, :] = sum_n Phi(x_m, y_n) val_n for x = qside rows.
-void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk,
-              const float* scal, const uint16_t* vks, const uint32_t* vslot, float* out) {
+// Forward-type pass: out[m, :] = sum_n Phi(x_m, y_n) val_n for x = qside rows
+// (out: byte stride os between problems).
+void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const float* scal,
+              const uint16_t* vks, const uint32_t* vslot, float* out, int64_t os) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
   const FwdK fk = fwd_for(p, dm);
-  PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT), fk.kernel);
-  FwdFn fn = fk.launch;
-  float* dst = ps.splits > 1 ? c.pl->part : out;
+  PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT), fk.kernel, c.pl->G);
+  const bool split = ps.splits > 1;
+  float* dst = split ? c.pl->part : out;
+  Bz bz = bz_ws(c);
+  bz.out = split ? c.slice : os;
   prof_before(kKindFwd, c.st);
-  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
-     ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)vks, vslot, c.tau2, nq, (int)p.C, ps.steps,
-     ps.sps, dst, ps.splits > 1 ? nq * p.C : 0);
+  fk.launch(grid_g(c, ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
+            ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)vks, vslot, c.tau2, nq, (int)p.C,
+            ps.steps, ps.sps, dst, split ? nq * p.C : 0, bz);
   prof_after(kKindFwd, c.st);
-  combine(c, ps, nq * p.C, out);
+  combine(c, ps, c.pl->part, nq * p.C, out, os);
 }
 
 // dq-type pass: out[m, :] = tau sum_n Phi(x_m, y_n) <gx_m, vy_n> (y_n - x_m).
-// g1 / g1_dt: the caller's single-channel upstream gradient of the query rows
-// (C = 1), read exactly in the epilogue.
+// g1 / g1_dt / g1s: the caller's single-channel upstream gradient of the
+// query rows (C = 1), read exactly in the epilogue, and its byte stride.
 // With out_s != NULL the forward sum over the same pairs is produced by the
-// same kernel (values vks: V^T in KS layout, unused for C = 1).
+// same kernel (values vks: V^T in KS layout, unused for C = 1).  os / os_s:
+// byte strides of out / out_s between problems.
 void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const float* scal,
              const uint32_t* kslot, const uint16_t* vrt, const uint32_t* vslot, const uint16_t* grt,
-             const uint32_t* gslot, const void* g1, gs_dtype g1_dt, float* out,
-             const uint16_t* vks = nullptr, float* out_s = nullptr) {
+             const uint32_t* gslot, const void* g1, gs_dtype g1_dt, int64_t g1s, float* out, int64_t os,
+             const uint16_t* vks = nullptr, float* out_s = nullptr, int64_t os_s = 0) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
   const bool fused = out_s != nullptr;
   const DqK dk = dq_for(p, dm, fused);
-  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, dq_cw(p, dm)), dk.kernel);
-  DqFn fn = dk.launch;
+  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, dq_cw(p, dm)), dk.kernel, c.pl->G);
   const bool split = ps.splits > 1;
   float* dst = split ? c.pl->part : out;
   float* dst_s = fused ? (split ? c.pl->part_s : out_s) : nullptr;
+  Bz bz = bz_ws(c);
+  bz.in2 = g1s;
+  bz.out = split ? c.slice : os;
+  bz.out2 = split ? c.slice : os_s;
   prof_before(kKindGrad, c.st);
-  fn(dim3(ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
-     ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)ks.ks,
-     p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot, (const uint4*)grt, gslot, g1,
-     (int)g1_dt, c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst, split ? nq * p.D : 0,
-     (const uint4*)vks, (int)p.C, dst_s, split ? nq * p.C : 0);
+  dk.launch(grid_g(c, ps.blocks, ps.splits), c.st, (const uint4*)qs.rt, qs.nh, (const uint4*)ks.samp_rt,
+            ks.samp_nh, (const uint4*)ks.rt, scal, (const uint4*)ks.ks,
+            p.qk_dtype == GS_BF16 ? kslot : nullptr, (const uint4*)vrt, vslot, (const uint4*)grt, gslot,
+            g1, (int)g1_dt, c.tau2, c.tau, nq, (int)p.D, ps.steps, ps.sps, dst, split ? nq * p.D : 0,
+            (const uint4*)vks, (int)p.C, dst_s, split ? nq * p.C : 0, bz);
   prof_after(kKindGrad, c.st);
-  combine(c, ps, nq * p.D, out);
-  if (fused && split)
-    hipLaunchKernelGGL(k_combine, dim3(grid1(nq * p.C)), dim3(256), 0, c.st,
-                       (const float*)c.pl->part_s, ps.splits, nq * p.C, out_s);
+  combine(c, ps, c.pl->part, nq * p.D, out, os);
+  if (fused) combine(c, ps, c.pl->part_s, nq * p.C, out_s, os_s);
 }
 
 void fill_zero(hipStream_t st, float* p, int64_t n) {
@@ -704,61 +753,121 @@ int gauss_sum_profile_stop(float* ms, int max) {
 namespace gs {
 namespace {
 
-size_t workspace_for(const gs_problem* p, bool fwd, int want_dq, int want_dk, int want_dv) {
+// Problems per launch group at most (grid.z).
+constexpr int64_t kMaxGroup = 65535;
+
+// Workspace for `count` problems of shape p in one launch group (count
+// capped at kMaxGroup); 0 when nothing would be computed.
+size_t workspace_for(const gs_problem* p, bool fwd, int want_dq, int want_dk, int want_dv,
+                     int64_t count = 1) {
   if (check_problem(p) != GS_SUCCESS) return 0;
-  if (p->M == 0 || p->N == 0) return 0;
+  if (p->M == 0 || p->N == 0 || count < 1) return 0;
   Want w = want_for(*p, fwd, want_dq != 0, want_dk != 0, want_dv != 0);
   if (!w.fwd && !w.dq && !w.dk && !w.dv) return 0;
+  const int64_t G = std::min(count, kMaxGroup);
   Plan pl;
-  make_plan(*p, w, false, nullptr, pl);
+  make_plan(*p, w, false, nullptr, pl, G);
   // the plan with q and k aliased never needs more than the separate one
-  return pl.total;
+  return (size_t)G * pl.total;
 }
 
-// Common body of the three compute entry points: validates everything, then
-// enqueues the prep kernels and the passes for the requested outputs (out:
-// forward sum, dq / dk / dv: gradients; NULL = not requested).
-gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
-              const void* dout, gs_dtype dout_dtype, float* out, float* dq, float* dk, float* dv,
-              void* workspace, size_t workspace_bytes, hipStream_t stream,
-              bool validate_only = false) {
+// Problems per launch group for `cnt` problems and the workspace given (at
+// least one problem's slice, checked by the caller): the most that fit,
+// then evened out over the groups that takes.  pl: the plan for that size.
+int64_t group_size(const gs_problem& p, const Want& w, bool alias, int64_t cnt, size_t bytes, Plan& pl) {
+  int64_t G = std::min(cnt, kMaxGroup);
+  for (;;) {
+    make_plan(p, w, alias, nullptr, pl, G);
+    if (G == 1 || (size_t)G * pl.total <= bytes) break;
+    G = std::max<int64_t>(1, std::min<int64_t>(G - 1, (int64_t)(bytes / pl.total)));
+  }
+  const int64_t even = ceil_div(cnt, ceil_div(cnt, G));
+  if (even < G) {
+    Plan pe;
+    make_plan(p, w, alias, nullptr, pe, even);
+    if ((size_t)even * pe.total <= bytes) {
+      pl = pe;
+      return even;
+    }
+  }
+  return G;
+}
+
+// Common body of the compute entry points.  b == NULL: one problem; else a
+// batch of b->count problems at the element strides of b.  Validates
+// everything (every problem's operand spans against each other and the
+// workspace) before anything is enqueued, then runs the problems in launch
+// groups: prep kernels and passes for the requested outputs (out: forward
+// sum, dq / dk / dv: gradients; NULL = not requested), each launch covering a
+// whole group on grid.z.
+gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void* k, const void* v,
+              float tau, const void* dout, gs_dtype dout_dtype, float* out, float* dq, float* dk,
+              float* dv, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   gs_status st = check_problem(p);
   if (st != GS_SUCCESS) return st;
   if ((st = check_tau(tau)) != GS_SUCCESS) return st;
-  const bool grads = dq || dk || dv;
-  if (grads && !valid_dtype(dout_dtype)) return GS_ERR_UNSUPPORTED;
   const int64_t M = p->M, N = p->N, D = p->D, C = p->C;
+  const bool grads = dq || dk || dv;
+  gs_batch one{};
+  one.count = 1;
+  if (b) {
+    if (b->count < 0 || b->q_stride < 0 || b->k_stride < 0 || b->v_stride < 0 || b->dout_stride < 0 ||
+        b->out_stride < 0 || b->dq_stride < 0 || b->dk_stride < 0 || b->dv_stride < 0)
+      return GS_ERR_BAD_SHAPE;
+    if (b->count == 0) return GS_SUCCESS;  // nothing to compute, no pointer is used
+    if (!out && !grads) return GS_ERR_NULL_POINTER;
+  }
+  const gs_batch& bt = b ? *b : one;
+  const int64_t cnt = bt.count;
+  if (grads && !valid_dtype(dout_dtype)) return GS_ERR_UNSUPPORTED;
   if (!out && !grads) return M == 0 && N == 0 ? GS_SUCCESS : GS_ERR_NULL_POINTER;
+  if (cnt > 1 && ((out && bt.out_stride < M * C) || (dq && bt.dq_stride < M * D) ||
+                  (dk && bt.dk_stride < N * D) || (dv && bt.dv_stride < N * C)))
+    return GS_ERR_BAD_SHAPE;
   if ((M > 0 && (!q || (grads && !dout))) || (N > 0 && (!k || !v))) return GS_ERR_NULL_POINTER;
-  const size_t vs = dsize(p->v_dtype), gsz = dsize(dout_dtype);
+  const int64_t vs = (int64_t)dsize(p->v_dtype), gsz = (int64_t)dsize(dout_dtype);
+  // (strides count elements, so every problem's pointers keep the alignment
+  // of the first one's)
   if ((M > 0 && (!aligned(q, 2) || (grads && !aligned(dout, gsz)))) ||
       (N > 0 && (!aligned(k, 2) || !aligned(v, vs))) || (out && !aligned(out, 4)) ||
       (dq && !aligned(dq, 4)) || (dk && !aligned(dk, 4)) || (dv && !aligned(dv, 4)))
     return GS_ERR_MISALIGNED;
-  Range in[4] = {range_of(q, M * D * 2), range_of(k, N * D * 2), range_of(v, N * C * (int64_t)vs),
-                 range_of(grads ? dout : nullptr, grads ? M * C * (int64_t)gsz : 0)};
-  Range outs[4] = {range_of(out, out ? M * C * 4 : 0), range_of(dq, dq ? M * D * 4 : 0),
-                   range_of(dk, dk ? N * D * 4 : 0), range_of(dv, dv ? N * C * 4 : 0)};
+  // operand spans over the whole batch
+  auto span = [&](const void* base, int64_t stride, int64_t esize, int64_t elems) {
+    return range_of(base, base ? ((cnt - 1) * stride + elems) * esize : 0);
+  };
+  const Range in[4] = {span(q, bt.q_stride, 2, M * D), span(k, bt.k_stride, 2, N * D),
+                       span(v, bt.v_stride, vs, N * C),
+                       span(grads ? dout : nullptr, bt.dout_stride, gsz, M * C)};
+  const Range outs[4] = {span(out, bt.out_stride, 4, out ? M * C : 0),
+                         span(dq, bt.dq_stride, 4, dq ? M * D : 0),
+                         span(dk, bt.dk_stride, 4, dk ? N * D : 0),
+                         span(dv, bt.dv_stride, 4, dv ? N * C : 0)};
   for (int a = 0; a < 4; ++a) {
-    for (int b = 0; b < 4; ++b)
-      if (overlap(outs[a], in[b])) return GS_ERR_ALIAS;
-    for (int b = a + 1; b < 4; ++b)
-      if (overlap(outs[a], outs[b])) return GS_ERR_ALIAS;
+    for (int c = 0; c < 4; ++c)
+      if (overlap(outs[a], in[c])) return GS_ERR_ALIAS;
+    for (int c = a + 1; c < 4; ++c)
+      if (overlap(outs[a], outs[c])) return GS_ERR_ALIAS;
   }
+  auto at_w = [](float* base, int64_t i, int64_t stride) -> float* {
+    return base ? base + i * stride : nullptr;
+  };
   if (M == 0 || N == 0) {
-    if (validate_only) return GS_SUCCESS;
     // Empty sums: every requested output is zero.
-    if (M > 0) {
-      fill_zero(stream, out, M * C);
-      fill_zero(stream, dq, M * D);
-    }
-    if (N > 0) {
-      fill_zero(stream, dk, N * D);
-      fill_zero(stream, dv, N * C);
+    for (int64_t i = 0; i < cnt; ++i) {
+      if (M > 0) {
+        fill_zero(stream, at_w(out, i, bt.out_stride), M * C);
+        fill_zero(stream, at_w(dq, i, bt.dq_stride), M * D);
+      }
+      if (N > 0) {
+        fill_zero(stream, at_w(dk, i, bt.dk_stride), N * D);
+        fill_zero(stream, at_w(dv, i, bt.dv_stride), N * C);
+      }
     }
     return launch_status();
   }
-  const bool alias = (q == k) && (M == N);
+  // the same array for q and k in every problem
+  const bool alias = (q == k) && (M == N) && (cnt == 1 || bt.q_stride == bt.k_stride);
   Want w = want_for(*p, out != nullptr, dq != nullptr, dk != nullptr, dv != nullptr);
   {
     // every kernel the passes below launch must exist for this shape
@@ -768,106 +877,69 @@ gs_status run(const gs_problem* p, const void* q, const void* k, const void* v, 
     if (w.dk && !dq_for(*p, dm, false).launch) return GS_ERR_INTERNAL;
   }
   Plan pl;
-  make_plan(*p, w, alias, nullptr, pl);
+  make_plan(*p, w, alias, nullptr, pl, 1);
   if ((st = check_workspace(workspace, workspace_bytes, pl.total)) != GS_SUCCESS) return st;
-  Range rw = range_of(workspace, (int64_t)pl.total);
+  const int64_t G = cnt > 1 ? group_size(*p, w, alias, cnt, workspace_bytes, pl) : 1;
+  const Range rw = range_of(workspace, G * (int64_t)pl.total);
   for (int a = 0; a < 4; ++a)
     if (overlap(outs[a], rw) || overlap(in[a], rw)) return GS_ERR_ALIAS;
-  if (validate_only) return GS_SUCCESS;
-  make_plan(*p, w, alias, workspace, pl);
+  make_plan(*p, w, alias, workspace, pl, G);
 
-  Ctx c{stream, p, &pl, tau, (float)(tau * 1.4426950408889634)};
-  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u);
-  const bool one = C == 1;
-  if (alias) {
-    // q.ks serves dk (keys q, signs of dout) unless only dq wants a KS copy
-    const bool q_for_dk = w.dk;
-    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one ? (q_for_dk ? dout : v) : nullptr,
-                q_for_dk ? dout_dtype : p->v_dtype);
-    if (pl.k.ks != pl.q.ks) prep_points_ks(c, k, N, pl.Np, pl.k.ks, pl.slots + 2, v, p->v_dtype);
-  } else {
-    prep_points(c, q, M, pl.Mp, pl.q, pl.slots + 2, one && grads ? dout : nullptr, dout_dtype);
-    prep_points(c, k, N, pl.Np, pl.k, pl.slots + 3, one ? v : nullptr, p->v_dtype);
-  }
-  if (w.fwd || w.dq || w.dk) prep_values(c, v, p->v_dtype, N, pl.Np, pl.v, pl.slots + 0);
-  // dout: its maximum scales the RT / KS copies (several channels, dv) and
-  // enters the key scalars of passes keyed by q (dk, dv); a single-channel dq
-  // reads dout exactly in its epilogue and needs none of it
-  if (grads && (C > 1 || w.dk || w.dv)) prep_values(c, dout, dout_dtype, M, pl.Mp, pl.g, pl.slots + 1);
-  if (pl.scal_kv) prep_scalars(c, pl.k, v, p->v_dtype, N, pl.Np, pl.slots + 0, pl.scal_kv);
-  if (pl.scal_qg) prep_scalars(c, pl.q, dout, dout_dtype, M, pl.Mp, pl.slots + 1, pl.scal_qg);
-  const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
-  // full-sample row-bound flags for the forward-kernel passes (fwd, dv)
-  if (w.fwd && !w.fused()) row_check(c, pl.q, M, pl.Mp, pl.k);
-  if (w.dv && !(alias && w.fwd && !w.fused())) row_check(c, pl.k, N, pl.Np, pl.q);
-  if (w.fwd && !w.fused()) pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out);
-  if (w.dq)
-    pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1,
-            dout, dout_dtype, dq, pl.v.ks, w.fused() ? out : nullptr);
-  if (w.dk)
-    pass_dq(c, pl.k, N, pl.q, M, pl.scal_qg, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt,
-            pl.slots + 0, v, p->v_dtype, dk);
-  if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv);
-  return launch_status();
-}
-
-
-// A batch of problems of one shape: every problem is validated first (its
-// pointers, and the spans of all outputs against the spans of all inputs,
-// the workspace and each other), then each runs through run() in order.
-gs_status run_batched(const gs_problem* p, const gs_batch* b, const void* q, const void* k,
-                      const void* v, float tau, const void* dout, gs_dtype dout_dtype, float* out,
-                      float* dq, float* dk, float* dv, void* workspace, size_t workspace_bytes,
-                      hipStream_t stream) {
-  gs_status st = check_problem(p);
-  if (st != GS_SUCCESS) return st;
-  if ((st = check_tau(tau)) != GS_SUCCESS) return st;
-  if (!b) return GS_ERR_NULL_POINTER;
-  const int64_t cnt = b->count, M = p->M, N = p->N, D = p->D, C = p->C;
-  if (cnt < 0 || b->q_stride < 0 || b->k_stride < 0 || b->v_stride < 0 || b->dout_stride < 0 ||
-      b->out_stride < 0 || b->dq_stride < 0 || b->dk_stride < 0 || b->dv_stride < 0)
-    return GS_ERR_BAD_SHAPE;
-  if (cnt == 0) return GS_SUCCESS;  // nothing to compute, no pointer is used
-  const bool grads = dq || dk || dv;
-  if (!out && !grads) return GS_ERR_NULL_POINTER;
-  if (grads && !valid_dtype(dout_dtype)) return GS_ERR_UNSUPPORTED;
-  const int64_t vs = (int64_t)dsize(p->v_dtype), gsz = (int64_t)dsize(dout_dtype);
-  if (cnt > 1 && ((out && b->out_stride < M * C) || (dq && b->dq_stride < M * D) ||
-                  (dk && b->dk_stride < N * D) || (dv && b->dv_stride < N * C)))
-    return GS_ERR_BAD_SHAPE;
-  // (strides count elements, so every problem's pointers keep the alignment
-  // of the first one's; the per-problem validation below checks it)
-  // spans over the whole batch
-  auto span = [&](const void* base, int64_t stride, int64_t esize, int64_t elems) {
-    return range_of(base, base ? ((cnt - 1) * stride + elems) * esize : 0);
+  // byte strides between problems
+  const int64_t qs = bt.q_stride * 2, ks = bt.k_stride * 2, vst = bt.v_stride * vs,
+                gst = bt.dout_stride * gsz, os = bt.out_stride * 4, dqs = bt.dq_stride * 4,
+                dks = bt.dk_stride * 4, dvs = bt.dv_stride * 4;
+  auto at = [](const void* base, int64_t i, int64_t bytes) -> const char* {
+    return base ? static_cast<const char*>(base) + i * bytes : nullptr;
   };
-  const Range in[4] = {span(q, b->q_stride, 2, M * D), span(k, b->k_stride, 2, N * D),
-                       span(v, b->v_stride, vs, N * C),
-                       span(grads ? dout : nullptr, b->dout_stride, gsz, M * C)};
-  const Range outs[4] = {span(out, b->out_stride, 4, M * C), span(dq, b->dq_stride, 4, M * D),
-                         span(dk, b->dk_stride, 4, N * D), span(dv, b->dv_stride, 4, N * C)};
-  for (int a = 0; a < 4; ++a) {
-    for (int c = 0; c < 4; ++c)
-      if (overlap(outs[a], in[c])) return GS_ERR_ALIAS;
-    for (int c = a + 1; c < 4; ++c)
-      if (overlap(outs[a], outs[c])) return GS_ERR_ALIAS;
-  }
-  auto at = [](const void* base, int64_t i, int64_t stride, int64_t esize) -> const char* {
-    return base ? static_cast<const char*>(base) + i * stride * esize : nullptr;
+  auto at_o = [](float* base, int64_t i, int64_t bytes) -> float* {
+    return base ? reinterpret_cast<float*>(reinterpret_cast<char*>(base) + i * bytes) : nullptr;
   };
-  auto at_w = [](float* base, int64_t i, int64_t stride) -> float* {
-    return base ? base + i * stride : nullptr;
-  };
-  for (int pass = 0; pass < 2; ++pass) {  // 0: validate every problem, 1: run them
-    for (int64_t i = 0; i < cnt; ++i) {
-      st = run(p, at(q, i, b->q_stride, 2), at(k, i, b->k_stride, 2), at(v, i, b->v_stride, vs), tau,
-               at(dout, i, b->dout_stride, gsz), dout_dtype, at_w(out, i, b->out_stride),
-               at_w(dq, i, b->dq_stride), at_w(dk, i, b->dk_stride), at_w(dv, i, b->dv_stride),
-               workspace, workspace_bytes, stream, pass == 0);
-      if (st != GS_SUCCESS) return st;
+  const bool one_c = C == 1;
+  const float tau2 = (float)(tau * 1.4426950408889634);
+  for (int64_t g0 = 0; g0 < cnt; g0 += G) {
+    Ctx c{stream, p, &pl, tau, tau2, (unsigned)std::min(G, cnt - g0), (int64_t)pl.total};
+    const void* q_ = at(q, g0, qs);
+    const void* k_ = at(k, g0, ks);
+    const void* v_ = at(v, g0, vst);
+    const void* g_ = grads ? at(dout, g0, gst) : nullptr;
+    float* out_ = at_o(out, g0, os);
+    float* dq_ = at_o(dq, g0, dqs);
+    float* dk_ = at_o(dk, g0, dks);
+    float* dv_ = at_o(dv, g0, dvs);
+    hipLaunchKernelGGL(k_fill_u32, grid_g(c, 1), dim3(64), 0, stream, pl.slots, 16, 0u, bz_ws(c));
+    if (alias) {
+      // q.ks serves dk (keys q, signs of dout) unless only dq wants a KS copy
+      const bool q_for_dk = w.dk;
+      prep_points(c, q_, qs, M, pl.Mp, pl.q, pl.slots + 2, one_c ? (q_for_dk ? g_ : v_) : nullptr,
+                  q_for_dk ? dout_dtype : p->v_dtype, q_for_dk ? gst : vst);
+      if (pl.k.ks != pl.q.ks)
+        prep_points_ks(c, k_, ks, N, pl.Np, pl.k.ks, pl.slots + 2, v_, p->v_dtype, vst);
+    } else {
+      prep_points(c, q_, qs, M, pl.Mp, pl.q, pl.slots + 2, one_c && grads ? g_ : nullptr, dout_dtype, gst);
+      prep_points(c, k_, ks, N, pl.Np, pl.k, pl.slots + 3, one_c ? v_ : nullptr, p->v_dtype, vst);
     }
+    if (w.fwd || w.dq || w.dk) prep_values(c, v_, p->v_dtype, vst, N, pl.Np, pl.v, pl.slots + 0);
+    // dout: its maximum scales the RT / KS copies (several channels, dv) and
+    // enters the key scalars of passes keyed by q (dk, dv); a single-channel
+    // dq reads dout exactly in its epilogue and needs none of it
+    if (grads && (C > 1 || w.dk || w.dv)) prep_values(c, g_, dout_dtype, gst, M, pl.Mp, pl.g, pl.slots + 1);
+    if (pl.scal_kv) prep_scalars(c, pl.k, v_, p->v_dtype, vst, N, pl.Np, pl.slots + 0, pl.scal_kv);
+    if (pl.scal_qg) prep_scalars(c, pl.q, g_, dout_dtype, gst, M, pl.Mp, pl.slots + 1, pl.scal_qg);
+    const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
+    // full-sample row-bound flags for the forward-kernel passes (fwd, dv)
+    if (w.fwd && !w.fused()) row_check(c, pl.q, M, pl.Mp, pl.k);
+    if (w.dv && !(alias && w.fwd && !w.fused())) row_check(c, pl.k, N, pl.Np, pl.q);
+    if (w.fwd && !w.fused()) pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out_, os);
+    if (w.dq)
+      pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1, g_,
+              dout_dtype, gst, dq_, dqs, pl.v.ks, w.fused() ? out_ : nullptr, os);
+    if (w.dk)
+      pass_dq(c, pl.k, N, pl.q, M, pl.scal_qg, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt,
+              pl.slots + 0, v_, p->v_dtype, vst, dk_, dks);
+    if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv_, dvs);
   }
-  return GS_SUCCESS;
+  return launch_status();
 }
 
 }  // namespace
@@ -892,7 +964,7 @@ gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const
     if (p && check_problem(p) == GS_SUCCESS && check_tau(tau) == GS_SUCCESS && p->M == 0)
       return GS_SUCCESS;
     if (!out && p) return GS_ERR_NULL_POINTER;
-    return run(p, q, k, v, tau, nullptr, GS_F32, out, nullptr, nullptr, nullptr, workspace,
+    return run(p, nullptr, q, k, v, tau, nullptr, GS_F32, out, nullptr, nullptr, nullptr, workspace,
                workspace_bytes, stream);
   } catch (...) {
     return GS_ERR_INTERNAL;
@@ -909,8 +981,8 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
       if ((st = check_tau(tau)) != GS_SUCCESS) return st;
       return GS_ERR_NULL_POINTER;
     }
-    return run(p, q, k, v, tau, dout, dout_dtype, nullptr, dq, dk, dv, workspace, workspace_bytes,
-               stream);
+    return run(p, nullptr, q, k, v, tau, dout, dout_dtype, nullptr, dq, dk, dv, workspace,
+               workspace_bytes, stream);
   } catch (...) {
     return GS_ERR_INTERNAL;
   }
@@ -927,8 +999,8 @@ gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, c
       if ((st = check_tau(tau)) != GS_SUCCESS) return st;
       return GS_ERR_NULL_POINTER;
     }
-    return run(p, q, k, v, tau, dout, dout_dtype, out, dq, dk, dv, workspace, workspace_bytes,
-               stream);
+    return run(p, nullptr, q, k, v, tau, dout, dout_dtype, out, dq, dk, dv, workspace,
+               workspace_bytes, stream);
   } catch (...) {
     return GS_ERR_INTERNAL;
   }
@@ -976,7 +1048,7 @@ gs_status gauss_sum_mmd_flow(const gs_problem* p, const void* x, const void* v, 
     float* s_out = s ? s : (mmd2 ? sbuf : nullptr);
     if (n > 0) {
       if (grad) hipLaunchKernelGGL(k_fill_f32, dim3(grid1(n)), dim3(256), 0, stream, ones, n, 1.0f);
-      st = run(p, x, x, v, tau, grad ? ones : nullptr, GS_F32, s_out, grad, nullptr, nullptr,
+      st = run(p, nullptr, x, x, v, tau, grad ? ones : nullptr, GS_F32, s_out, grad, nullptr, nullptr,
                base + extra, workspace_bytes - extra, stream);
       if (st != GS_SUCCESS) return st;
     }
@@ -991,12 +1063,36 @@ gs_status gauss_sum_mmd_flow(const gs_problem* p, const void* x, const void* v, 
     return GS_ERR_INTERNAL;
   }
 }
+size_t gauss_sum_fwd_batched_workspace_size(const gs_problem* p, int64_t count) {
+  try {
+    return workspace_for(p, true, 0, 0, 0, count);
+  } catch (...) {
+    return 0;
+  }
+}
+
+size_t gauss_sum_bwd_batched_workspace_size(const gs_problem* p, int64_t count, int want_dq,
+                                            int want_dk, int want_dv) {
+  if (!want_dq && !want_dk && !want_dv) return 0;
+  try {
+    return workspace_for(p, false, want_dq, want_dk, want_dv, count);
+  } catch (...) {
+    return 0;
+  }
+}
+
 gs_status gauss_sum_fwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
                                 const void* k, const void* v, float tau, float* out,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
-    return run_batched(p, batch, q, k, v, tau, nullptr, GS_F32, out, nullptr, nullptr, nullptr,
-                       workspace, workspace_bytes, stream);
+    if (!batch) {
+      gs_status st = check_problem(p);
+      if (st != GS_SUCCESS) return st;
+      if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+      return GS_ERR_NULL_POINTER;
+    }
+    return run(p, batch, q, k, v, tau, nullptr, GS_F32, out, nullptr, nullptr, nullptr, workspace,
+               workspace_bytes, stream);
   } catch (...) {
     return GS_ERR_INTERNAL;
   }
@@ -1007,8 +1103,14 @@ gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, cons
                                 gs_dtype dout_dtype, float* dq, float* dk, float* dv,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
-    return run_batched(p, batch, q, k, v, tau, dout, dout_dtype, nullptr, dq, dk, dv, workspace,
-                       workspace_bytes, stream);
+    if (!batch) {
+      gs_status st = check_problem(p);
+      if (st != GS_SUCCESS) return st;
+      if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+      return GS_ERR_NULL_POINTER;
+    }
+    return run(p, batch, q, k, v, tau, dout, dout_dtype, nullptr, dq, dk, dv, workspace,
+               workspace_bytes, stream);
   } catch (...) {
     return GS_ERR_INTERNAL;
   }

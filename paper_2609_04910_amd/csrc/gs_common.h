@@ -108,6 +108,28 @@ __device__ __forceinline__ int scale_exponent(uint32_t max_bits) {
   return 1 - e;
 }
 
+// Per-problem byte strides of a launch over a batch of problems: problem
+// blockIdx.z finds each operand at its base + blockIdx.z * stride.  One
+// problem: all zero, gridDim.z = 1.
+struct Bz {
+  int64_t ws = 0;    // the problem's workspace slice (every derived operand)
+  int64_t in = 0;    // the caller's input array the kernel reads
+  int64_t in2 = 0;   // a second caller input (sign source of a KS copy, exact upstream gradient)
+  int64_t out = 0;   // output: the caller's array, or the partial sums in the workspace
+  int64_t out2 = 0;  // second output (forward sum of a fused gradient pass)
+};
+
+// p advanced to problem blockIdx.z (NULL stays NULL).
+template <typename P>
+__device__ __forceinline__ const P* zoff(const P* p, int64_t stride) {
+  return p ? reinterpret_cast<const P*>(reinterpret_cast<const char*>(p) + (int64_t)blockIdx.z * stride)
+           : p;
+}
+template <typename P>
+__device__ __forceinline__ P* zoff(P* p, int64_t stride) {
+  return p ? reinterpret_cast<P*>(reinterpret_cast<char*>(p) + (int64_t)blockIdx.z * stride) : p;
+}
+
 // RT-layout half index of element (r, w) for a matrix with W (multiple of 32) columns.
 __host__ __device__ __forceinline__ int64_t rt_index(int64_t r, int w, int W) {
   return (((r >> 4) * (W >> 5) + (w >> 5)) * 16 + (r & 15)) * 32 + (w & 31);

@@ -196,8 +196,13 @@ __device__ __forceinline__ bool needs_shift(const uint4* __restrict__ sample_rt,
 template <typename T, int DP>
 __global__ __launch_bounds__(kBlockThreads) void k_row_check(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ sample_rt,
-    const float* __restrict__ sample_nh, float tau2, int64_t M, uint32_t* __restrict__ shift) {
+    const float* __restrict__ sample_nh, float tau2, int64_t M, uint32_t* __restrict__ shift, Bz bz) {
   constexpr int QT = 4;
+  qs = zoff(qs, bz.ws);
+  nhq = zoff(nhq, bz.ws);
+  sample_rt = zoff(sample_rt, bz.ws);
+  sample_nh = zoff(sample_nh, bz.ws);
+  shift = zoff(shift, bz.ws);
   const int lane = threadIdx.x & (kWave - 1);
   const int j = lane & 15, g = lane >> 4;
   const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave) * (16 * QT);
@@ -306,12 +311,26 @@ __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
 // ONE (single channel, C = 1): the magnitude of v_n enters the exponent via the
 // step scalars (log2 |v_n 2^e| added to the key bias, max |v 2^e| in
 // [0.5, 1)) and V^T holds only the signs, so v contributes no fp16 rounding.
-template <typename T, int DP, int CT, int QT, bool ONE>
+//
+// BZ: a batch of problems on grid.z (operands at the strides of bz); the
+// instance for one problem never reads bz.
+template <typename T, int DP, int CT, int QT, bool ONE, bool BZ>
 __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
     const uint4* __restrict__ vt, const uint32_t* __restrict__ vslot, float tau2, int64_t M, int C,
-    int steps_total, int steps_per_split, float* __restrict__ out, int64_t part_stride) {
+    int steps_total, int steps_per_split, float* __restrict__ out, int64_t part_stride, Bz bz) {
+  if constexpr (BZ) {
+    qs = zoff(qs, bz.ws);
+    nhq = zoff(nhq, bz.ws);
+    samp_rt = zoff(samp_rt, bz.ws);
+    samp_nh = zoff(samp_nh, bz.ws);
+    ks = zoff(ks, bz.ws);
+    scal = zoff(scal, bz.ws);
+    vt = zoff(vt, bz.ws);
+    vslot = zoff(vslot, bz.ws);
+    out = zoff(out, bz.out);
+  }
   constexpr int KCH = 2 * DP;   // 1-KiB chunks of keys per step
   constexpr int NCH = KCH + CT; // + chunks of V^T
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
@@ -432,7 +451,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 // per CU: the large-D / large-C instances would otherwise take a few more
 // registers and run one wave per SIMD, which costs far more than the spill
 // of a few values outside the key loop.
-template <typename T, int DP, int CW, int QT, int FCT>
+template <typename T, int DP, int CW, int QT, int FCT, bool BZ>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_dq(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
@@ -441,7 +460,25 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
     const uint32_t* __restrict__ gslot, const void* __restrict__ g1, int g1_dtype, float tau2,
     float tau, int64_t M, int D, int steps_total, int steps_per_split, float* __restrict__ out,
     int64_t part_stride, const uint4* __restrict__ vt, int C, float* __restrict__ out_s,
-    int64_t part_stride_s) {
+    int64_t part_stride_s, Bz bz) {
+  if constexpr (BZ) {
+    qs = zoff(qs, bz.ws);
+    nhq = zoff(nhq, bz.ws);
+    samp_rt = zoff(samp_rt, bz.ws);
+    samp_nh = zoff(samp_nh, bz.ws);
+    ks = zoff(ks, bz.ws);
+    scal = zoff(scal, bz.ws);
+    kt_ks = zoff(kt_ks, bz.ws);
+    kslot = zoff(kslot, bz.ws);
+    vs = zoff(vs, bz.ws);
+    vslot = zoff(vslot, bz.ws);
+    gs = zoff(gs, bz.ws);
+    gslot = zoff(gslot, bz.ws);
+    vt = zoff(vt, bz.ws);
+    g1 = zoff(g1, bz.in2);
+    out = zoff(out, bz.out);
+    out_s = zoff(out_s, bz.out2);
+  }
   constexpr int DT = 2 * DP;                // 16-row tiles of K^T (KS layout)
   constexpr int KCH = 2 * DP;               // chunks of K (RT) per step
   constexpr int VCH = 2 * CW;               // chunks of V (RT) per step

@@ -15,7 +15,8 @@
 
 namespace gs {
 
-__global__ void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t val) {
+__global__ void k_fill_u32(uint32_t* __restrict__ p, int n, uint32_t val, Bz bz) {
+  p = zoff(p, bz.ws);
   int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = val;
 }
@@ -31,8 +32,10 @@ __global__ void k_fill_f32(float* __restrict__ p, int64_t n, float val) {
 // comparison of the bit patterns orders them; NaN compares largest).  Reduced
 // within the workgroup first: one atomic per workgroup.
 __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
-                         uint32_t* __restrict__ slot) {
+                         uint32_t* __restrict__ slot, Bz bz) {
   __shared__ uint32_t wmax[kWavesPerBlock];
+  x = zoff(x, bz.in);
+  slot = zoff(slot, bz.ws);
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
   uint32_t mb = 0;
@@ -70,7 +73,10 @@ __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
 // loop and the shuffles see whole waves.
 template <typename T>
 __global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad,
-                                 int W, uint16_t* __restrict__ xs, float* __restrict__ nh) {
+                                 int W, uint16_t* __restrict__ xs, float* __restrict__ nh, Bz bz) {
+  x = zoff(x, bz.in);
+  xs = zoff(xs, bz.ws);
+  nh = zoff(nh, bz.ws);
   const int cpr = W >> 3;  // threads per row (4, 8, 16 or 32)
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * cpr; t += stride) {
@@ -104,7 +110,11 @@ __global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int 
 template <typename T>
 __global__ void k_points_ks(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad, int R,
                             const uint32_t* __restrict__ slot, const void* __restrict__ sgn,
-                            int sgn_dtype, uint16_t* __restrict__ xt) {
+                            int sgn_dtype, uint16_t* __restrict__ xt, Bz bz) {
+  x = zoff(x, bz.in);
+  slot = zoff(slot, bz.ws);
+  sgn = zoff(sgn, bz.in2);
+  xt = zoff(xt, bz.ws);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float s = slot ? ldexpf(1.0f, scale_exponent(*slot)) : 1.0f;
   const int64_t total = (n_pad >> 5) * R * 4;
@@ -134,7 +144,11 @@ __global__ void k_points_ks(const uint16_t* __restrict__ x, int64_t n, int D, in
 // Values (fp32 / fp16 / bf16) scaled by 2^e(*slot) into fp16, RT layout
 // (W = C padded to 32) and / or KS layout (R = C padded to 16).
 __global__ void k_values_rt(const void* __restrict__ v, int dtype, int64_t n, int C, int64_t n_pad,
-                            int W, const uint32_t* __restrict__ slot, uint16_t* __restrict__ vs) {
+                            int W, const uint32_t* __restrict__ slot, uint16_t* __restrict__ vs,
+                            Bz bz) {
+  v = zoff(v, bz.in);
+  slot = zoff(slot, bz.ws);
+  vs = zoff(vs, bz.ws);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float s = ldexpf(1.0f, scale_exponent(*slot));
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * W; t += stride) {
@@ -150,7 +164,10 @@ __global__ void k_values_rt(const void* __restrict__ v, int dtype, int64_t n, in
 // through the step scalars) row 0 holds sign(v) = +-1 instead.
 __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, int C, int64_t n_pad,
                             int R, const uint32_t* __restrict__ slot, int sign_only,
-                            uint16_t* __restrict__ vt) {
+                            uint16_t* __restrict__ vt, Bz bz) {
+  v = zoff(v, bz.in);
+  slot = zoff(slot, bz.ws);
+  vt = zoff(vt, bz.ws);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float s = ldexpf(1.0f, scale_exponent(*slot));
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * R; t += stride) {
@@ -174,8 +191,12 @@ __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, in
 // (k_points_rt_norm), copied so that sampled and streamed keys agree exactly.
 __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W,
                          const float* __restrict__ nh, uint16_t* __restrict__ srt,
-                         float* __restrict__ snh) {
+                         float* __restrict__ snh, Bz bz) {
   constexpr int kStride = kSampleRows / kSampleCoarse;
+  x = zoff(x, bz.in);
+  nh = zoff(nh, bz.ws);
+  srt = zoff(srt, bz.ws);
+  snh = zoff(snh, bz.ws);
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= kSampleRows * W) return;
   const int pos = t / W, w = t - (t / W) * W;
@@ -203,7 +224,11 @@ __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W
 //   [48, 64) unused, 0.
 __global__ void k_step_scalars(const float* __restrict__ nh, const void* __restrict__ v, int dtype,
                                int64_t n, int64_t n_pad, const uint32_t* __restrict__ slot, float tau2,
-                               float* __restrict__ out) {
+                               float* __restrict__ out, Bz bz) {
+  nh = zoff(nh, bz.ws);
+  v = zoff(v, bz.in);
+  slot = zoff(slot, bz.ws);
+  out = zoff(out, bz.ws);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float sc = v ? ldexpf(1.0f, scale_exponent(*slot) - 1) : 0.0f;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * 2; t += stride) {
@@ -259,7 +284,9 @@ __global__ void k_dot_final(const double* __restrict__ part, int parts, double* 
 // elements per thread where count allows 16-byte accesses, the loads of up to
 // eight splits issued together before they are added in order.
 __global__ void k_combine(const float* __restrict__ part, int splits, int64_t count,
-                          float* __restrict__ out) {
+                          float* __restrict__ out, Bz bz) {
+  part = zoff(part, bz.ws);
+  out = zoff(out, bz.out);
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   if ((count & 3) == 0) {

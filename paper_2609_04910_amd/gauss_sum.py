@@ -31,7 +31,8 @@ EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_bwd", "gauss_sum_fw
             "gauss_sum_bwd_workspace_size", "gauss_sum_fwd_bwd_workspace_size",
             "gauss_sum_status_string", "gauss_sum_abi_version", "gauss_sum_profile_start",
             "gauss_sum_profile_stop", "gauss_sum_mmd_flow", "gauss_sum_mmd_flow_workspace_size",
-            "gauss_sum_fwd_batched", "gauss_sum_bwd_batched")
+            "gauss_sum_fwd_batched", "gauss_sum_bwd_batched", "gauss_sum_fwd_batched_workspace_size",
+            "gauss_sum_bwd_batched_workspace_size")
 PROFILE_FWD, PROFILE_GRAD = 1, 2
 
 
@@ -87,6 +88,11 @@ def load(path=LIB_PATH):
     lib.gauss_sum_bwd_batched.argtypes = [P, BP, vp, vp, vp, ctypes.c_float, vp, ctypes.c_int, f32p,
                                           f32p, f32p, vp, sz, vp]
     lib.gauss_sum_bwd_batched.restype = ctypes.c_int
+    lib.gauss_sum_fwd_batched_workspace_size.argtypes = [P, ctypes.c_int64]
+    lib.gauss_sum_fwd_batched_workspace_size.restype = sz
+    lib.gauss_sum_bwd_batched_workspace_size.argtypes = [P, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                                         ctypes.c_int]
+    lib.gauss_sum_bwd_batched_workspace_size.restype = sz
     lib.gauss_sum_mmd_flow.argtypes = [P, vp, vp, ctypes.c_float, f32p, f32p, vp, vp, sz, vp]
     lib.gauss_sum_mmd_flow.restype = ctypes.c_int
     lib.gauss_sum_mmd_flow_workspace_size.argtypes = [P]
@@ -291,9 +297,22 @@ def _batched_inputs(q, k, v):
     return B, M, N, D, C, M * D, ks, vs
 
 
-def gauss_sum_fwd_batched(q, k, v, tau, out=None, workspace=None, stream=None):
+def gauss_sum_fwd_batched_workspace_size(M, N, D, C, count, qk_dtype=GS_F16, v_dtype=GS_F32):
+    p = make_problem(M, N, D, C, qk_dtype, v_dtype)
+    return int(load().gauss_sum_fwd_batched_workspace_size(ctypes.byref(p), int(count)))
+
+
+def gauss_sum_bwd_batched_workspace_size(M, N, D, C, count, qk_dtype=GS_F16, v_dtype=GS_F32,
+                                         want_dq=True, want_dk=True, want_dv=True):
+    p = make_problem(M, N, D, C, qk_dtype, v_dtype)
+    return int(load().gauss_sum_bwd_batched_workspace_size(ctypes.byref(p), int(count), int(bool(want_dq)),
+                                                           int(bool(want_dk)), int(bool(want_dv))))
+
+
+def gauss_sum_fwd_batched(q, k, v, tau, out=None, workspace=None, stream=None, group=None):
     """B independent forward sums: q is B x M x D, k and v are B x N x (D, C)
-    or shared N x (D, C); returns B x M x C fp32."""
+    or shared N x (D, C); returns B x M x C fp32.  Without a workspace, one is
+    allocated for `group` problems per launch (default: all B)."""
     import torch
     B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
     p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
@@ -301,7 +320,7 @@ def gauss_sum_fwd_batched(q, k, v, tau, out=None, workspace=None, stream=None):
     if out is None:
         out = torch.empty((B, M, C), dtype=torch.float32, device=q.device)
     b = Batch(B, qs, ks, vs, 0, M * C, 0, 0, 0)
-    need = int(lib.gauss_sum_fwd_workspace_size(ctypes.byref(p)))
+    need = int(lib.gauss_sum_fwd_batched_workspace_size(ctypes.byref(p), int(group or max(B, 1))))
     if workspace is None:
         workspace, wbytes = _workspace(need, q.device)
     else:
@@ -313,9 +332,12 @@ def gauss_sum_fwd_batched(q, k, v, tau, out=None, workspace=None, stream=None):
     return out
 
 
-def gauss_sum_bwd_batched(q, k, v, tau, dout, want=(True, True, True), workspace=None, stream=None):
+def gauss_sum_bwd_batched(q, k, v, tau, dout, want=(True, True, True), workspace=None, stream=None,
+                          group=None):
     """Gradients of B independent problems (q, k shared as in
-    gauss_sum_fwd_batched; dout is B x M x C); each output B x (rows) x (D or C)."""
+    gauss_sum_fwd_batched; dout is B x M x C); each output B x (rows) x (D or C).
+    Without a workspace, one is allocated for `group` problems per launch
+    (default: all B)."""
     import torch
     B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
     if not dout.is_cuda or dout.shape != (B, M, C) or not dout.is_contiguous():
@@ -329,8 +351,9 @@ def gauss_sum_bwd_batched(q, k, v, tau, dout, want=(True, True, True), workspace
     dk = torch.empty((B, N, D), dtype=torch.float32, device=dev) if want[1] else None
     dv = torch.empty((B, N, C), dtype=torch.float32, device=dev) if want[2] else None
     b = Batch(B, qs, ks, vs, M * C, 0, M * D, N * D, N * C)
-    need = int(lib.gauss_sum_bwd_workspace_size(ctypes.byref(p), int(bool(want[0])),
-                                                int(bool(want[1])), int(bool(want[2]))))
+    need = int(lib.gauss_sum_bwd_batched_workspace_size(ctypes.byref(p), int(group or max(B, 1)),
+                                                        int(bool(want[0])), int(bool(want[1])),
+                                                        int(bool(want[2]))))
     if workspace is None:
         workspace, wbytes = _workspace(need, dev)
     else:

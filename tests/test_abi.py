@@ -196,6 +196,26 @@ def test_workspace_sizes():
     assert flow % 256 == 0
 
 
+def test_batched_workspace_sizes():
+    # one problem per group: exactly the single-problem workspace
+    assert gs.gauss_sum_fwd_batched_workspace_size(1000, 3000, 64, 4, 1) == \
+        gs.gauss_sum_fwd_workspace_size(1000, 3000, 64, 4)
+    assert gs.gauss_sum_bwd_batched_workspace_size(1000, 3000, 64, 4, 1) == \
+        gs.gauss_sum_bwd_workspace_size(1000, 3000, 64, 4)
+    one = gs.gauss_sum_fwd_workspace_size(16384, 16384, 32, 1)
+    many = gs.gauss_sum_fwd_batched_workspace_size(16384, 16384, 32, 1, 64)
+    # 64 slices, each at most the single-problem one (fewer key splits)
+    assert 0 < many <= 64 * one and many % (64 * 256) == 0 and many > one
+    assert gs.gauss_sum_fwd_batched_workspace_size(64, 64, 8, 1, 0) == 0
+    assert gs.gauss_sum_fwd_batched_workspace_size(0, 64, 8, 1, 4) == 0
+    assert gs.gauss_sum_fwd_batched_workspace_size(64, 64, 0, 1, 4) == 0
+    assert gs.gauss_sum_bwd_batched_workspace_size(64, 64, 8, 1, 4, want_dq=False, want_dk=False,
+                                                   want_dv=False) == 0
+    # groups stop at 65535 problems
+    assert gs.gauss_sum_fwd_batched_workspace_size(64, 64, 8, 1, 1 << 20) == \
+        gs.gauss_sum_fwd_batched_workspace_size(64, 64, 8, 1, 65535)
+
+
 def test_profile_hook_arguments():
     lib = gs.load()
     assert lib.gauss_sum_profile_start(0, 1) == 2
