@@ -292,6 +292,144 @@ def bench_batched(args):
     print(json.dumps(res), flush=True)
 
 
+def compare_attention(args):
+    """The paper's route on this GPU, as an external comparison (it is not part
+    of the library and nothing in the library calls it): Alg. 1 (prescale:
+    fused attention with its log-sum-exp, values pre-multiplied by
+    exp(-tau/2 |k|^2), output rescaled by exp(lse - tau/2 |q|^2)) and Alg. 2
+    (reweight: queries and keys extended by two entries, one auxiliary key and
+    value channel with kappa = sqrt(N + 1), output kappa alpha / beta), both
+    through PyTorch's fused fp16 attention kernels (flash and
+    memory-efficient backends) with q and k shifted by their common mean and
+    the widths padded to multiples of 8 (Sec. 2, Remark 1).  Forward sums of
+    the batched workload; each route is timed like the library (settle,
+    warm-up, timed steps between events) and checked against the fp64 oracle
+    on sampled rows of three problems (relative L2 error).  Prints one JSON
+    line."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    import oracle
+    from paper_2609_04910_amd import gauss_sum as gs
+    from paper_2609_04910_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    q, k, v, tau = wl.make_batch(args.workload, seed=0)
+    tau = float(tau)
+    B, M, D = q.shape
+    N, C = v.shape[1], v.shape[2]
+    tq, tk, tv = (torch.from_numpy(a).to(dev) for a in (q, k, v))
+    stream = torch.cuda.current_stream()
+    ceil8 = lambda x: (x + 7) // 8 * 8
+
+    def centred():
+        mu = torch.cat([tq, tk], 1).float().mean(dim=1, keepdim=True)
+        qc = (tq.float() - mu).half()
+        kc = (tk.float() - mu).half()
+        return qc, kc, qc.float().pow(2).sum(-1), kc.float().pow(2).sum(-1)
+
+    def pad(x, width):
+        return F.pad(x, (0, width - x.shape[-1]))
+
+    def prescale(backend):
+        qc, kc, nq, nk = centred()
+        w = ceil8(max(D, C))
+        vt = (tv * torch.exp(-0.5 * tau * nk).unsqueeze(-1)).half()
+        Q, K, V = (pad(x, w).unsqueeze(1).contiguous() for x in (qc, kc, vt))
+        if backend == "flash":
+            r = torch.ops.aten._scaled_dot_product_flash_attention(Q, K, V, 0.0, False, False, scale=tau)
+        else:
+            r = torch.ops.aten._scaled_dot_product_efficient_attention(Q, K, V, None, True, 0.0, False,
+                                                                       scale=tau)
+        o, lse = r[0][:, 0, :, :C].float(), r[1][:, 0, :M].float()
+        return o * torch.exp(lse - 0.5 * tau * nq).unsqueeze(-1)
+
+    kappa = float(np.sqrt(N + 1))
+
+    def reweight(backend):
+        qc, kc, nq, nk = centred()
+        w = ceil8(max(D + 2, C + 1))
+        Q = torch.zeros((B, M, w), dtype=torch.float16, device=dev)
+        Q[..., :D] = qc
+        Q[..., D] = 1.0
+        Q[..., D + 1] = (0.5 * nq).half()
+        K = torch.zeros((B, N + 1, w), dtype=torch.float16, device=dev)
+        K[:, 0, D + 1] = 1.0
+        K[:, 1:, :D] = kc
+        K[:, 1:, D] = (-0.5 * nk).half()
+        V = torch.zeros((B, N + 1, w), dtype=torch.float16, device=dev)
+        V[:, 1:, :C] = tv.half()
+        V[:, 0, C] = kappa
+        be = SDPBackend.FLASH_ATTENTION if backend == "flash" else SDPBackend.EFFICIENT_ATTENTION
+        with sdpa_kernel([be]):
+            o = F.scaled_dot_product_attention(Q.unsqueeze(1), K.unsqueeze(1), V.unsqueeze(1), scale=tau)
+        o = o[:, 0].float()
+        return kappa * o[..., :C] / o[..., C:C + 1]
+
+    ws = torch.empty(max(gs.gauss_sum_fwd_batched_workspace_size(M, N, D, C, B), 1), dtype=torch.uint8,
+                     device=dev)
+    out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
+
+    def library():
+        gs.gauss_sum_fwd_batched(tq, tk, tv, tau, out=out, workspace=ws, stream=stream)
+        return out
+
+    rows = wl.sample_rows(M, 512, seed=3)
+    probs = (0, B // 2 + 1, B - 1)
+    refs = [oracle.fwd(q[b], k[b], v[b], tau, rows=rows, threads=min(oracle.default_threads(), 16))[0]
+            for b in probs]
+
+    def measure(fn):
+        res = fn()
+        torch.cuda.synchronize()
+        got = res.cpu().numpy()
+        num = sum(float(np.sum((got[b][rows].astype(np.float64) - r) ** 2)) for b, r in zip(probs, refs))
+        den = sum(float(np.sum(r ** 2)) for r in refs)
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < args.settle_ms:
+            fn()
+            torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        return {"ms_per_step": ms, "pairs_per_s": B * float(M) * N / (ms * 1e-3),
+                "rel_l2": float(np.sqrt(num / den)), "peak_mem_gib": None}
+
+    routes = {}
+    for name, fn in (("gauss_sum_fwd_batched", library),
+                     ("alg1_prescale_flash", lambda: prescale("flash")),
+                     ("alg1_prescale_mem_efficient", lambda: prescale("efficient")),
+                     ("alg2_reweight_flash", lambda: reweight("flash")),
+                     ("alg2_reweight_mem_efficient", lambda: reweight("efficient"))):
+        print("route", name, flush=True, file=sys.stderr)
+        try:
+            torch.cuda.reset_peak_memory_stats()
+            base = torch.cuda.memory_allocated()
+            routes[name] = measure(fn)
+            routes[name]["peak_mem_gib"] = (torch.cuda.max_memory_allocated() - base) / 2 ** 30
+        except RuntimeError as e:  # a backend that does not take these shapes here
+            routes[name] = {"error": str(e).splitlines()[0][:200]}
+    lib_ms = routes["gauss_sum_fwd_batched"]["ms_per_step"]
+    for r in routes.values():
+        if "ms_per_step" in r:
+            r["library_speedup"] = r["ms_per_step"] / lib_ms
+    print(json.dumps({"mode": "compare_attention", "unit": "pairs/s", "data": "synthetic",
+                      "config": {"workload": args.workload, "B": B, "M": M, "N": N, "D": D, "C": C,
+                                 "tau": tau, "passes": "fwd", "inputs": "f16 points, f32 values",
+                                 "accuracy": "rel-L2 vs fp64 oracle, 512 rows of problems %s" % (probs,)},
+                      "steps": args.steps, "warmup": args.warmup, "routes": routes}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -310,6 +448,9 @@ def main():
     ap.add_argument("--flow", action="store_true",
                     help="mmd_flow: time one gauss_sum_mmd_flow call per step (s, the flow field "
                          "and MMD^2 = v^T s) instead of gauss_sum_fwd_bwd")
+    ap.add_argument("--compare-attention", action="store_true",
+                    help="batched workloads: time the paper's attention route (Alg. 1 and 2 through "
+                         "PyTorch's fused attention) beside the library, forward only")
     ap.add_argument("--separate", action="store_true",
                     help="time separate gauss_sum_fwd + gauss_sum_bwd calls instead of one "
                          "gauss_sum_fwd_bwd call")
@@ -337,6 +478,12 @@ def main():
     gs.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.compare_attention:
+        if args.workload not in wl.BATCHED:
+            print("--compare-attention takes a batched workload (--workload batch_d32)", file=sys.stderr)
+            sys.exit(2)
+        compare_attention(args)
+        return
     if args.workload in wl.BATCHED:
         bench_batched(args)
         return
