@@ -468,8 +468,10 @@ void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t xs, int64_t n, int
   Bz bz = bz_ws(c);
   bz.in = xs;
   bz.in2 = sgns;
+  // 16-byte row loads when every problem's rows start on 16-byte boundaries
+  const int vec = (p.D % 8 == 0) && ((reinterpret_cast<uintptr_t>(x16) | (uintptr_t)xs) % 16 == 0);
   hipLaunchKernelGGL(k_points_rt_norm<T>, grid_g(c, grid1(n_pad * (W / 8))), dim3(256), 0, c.st, x16, n,
-                     (int)p.D, n_pad, W, s.rt, s.nh, bz);
+                     (int)p.D, n_pad, W, s.rt, s.nh, vec, bz);
   if (s.samp_rt)
     hipLaunchKernelGGL(k_sample, grid_g(c, grid1(kSampleRows * W)), dim3(256), 0, c.st, x16, n, (int)p.D,
                        W, (const float*)s.nh, s.samp_rt, s.samp_nh, bz);
@@ -525,7 +527,7 @@ void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t xs, int64_t n
     hipLaunchKernelGGL(k_values_rt, grid_g(c, grid1(n_pad * Wv)), dim3(256), 0, c.st, x, (int)dt, n,
                        (int)p.C, n_pad, Wv, (const uint32_t*)slot, s.rt, bz);
   if (s.ks)
-    hipLaunchKernelGGL(k_values_ks, grid_g(c, grid1(n_pad * Rv)), dim3(256), 0, c.st, x, (int)dt, n,
+    hipLaunchKernelGGL(k_values_ks, grid_g(c, grid1(n_pad / 8 * Rv)), dim3(256), 0, c.st, x, (int)dt, n,
                        (int)p.C, n_pad, Rv, (const uint32_t*)slot, (int)(p.C == 1), s.ks, bz);
 }
 

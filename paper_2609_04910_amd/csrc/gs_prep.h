@@ -70,10 +70,13 @@ __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
 // nh[r] = -||x_r||^2 / 2 is rounded once to fp32.  Padding rows / columns are
 // zero, padding rows get kPadBias.  n_pad * W/8 is a multiple of the wave
 // size, so every lane of a wave runs the same iterations of the grid-stride
-// loop and the shuffles see whole waves.
+// loop and the shuffles see whole waves.  vec: rows start on 16-byte
+// boundaries and D is a multiple of 8, so the eight columns are one 16-byte
+// load.
 template <typename T>
 __global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad,
-                                 int W, uint16_t* __restrict__ xs, float* __restrict__ nh, Bz bz) {
+                                 int W, uint16_t* __restrict__ xs, float* __restrict__ nh, int vec,
+                                 Bz bz) {
   x = zoff(x, bz.in);
   xs = zoff(xs, bz.ws);
   nh = zoff(nh, bz.ws);
@@ -83,11 +86,22 @@ __global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int 
     const int64_t r = t / cpr;
     const int c = (int)(t - r * cpr);
     uint16_t h[8];
+    if (vec) {
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (r < n && 8 * c < D) u = *reinterpret_cast<const uint4*>(x + r * D + 8 * c);
+      const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h[e] = (uint16_t)(wd[e >> 1] >> (16 * (e & 1)));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int w = 8 * c + e;
+        h[e] = (r < n && w < D) ? x[r * D + w] : (uint16_t)0;
+      }
+    }
     double acc = 0.0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int w = 8 * c + e;
-      h[e] = (r < n && w < D) ? x[r * D + w] : (uint16_t)0;
       const double v = (double)T::to_float(h[e]);
       acc += v * v;
     }
@@ -161,7 +175,9 @@ __global__ void k_values_rt(const void* __restrict__ v, int dtype, int64_t n, in
 }
 
 // With sign_only (single-channel values, whose magnitudes enter the exponent
-// through the step scalars) row 0 holds sign(v) = +-1 instead.
+// through the step scalars) row 0 holds sign(v) = +-1 instead.  Thread
+// (32-key block, row w, quarter a) writes the eight key slots 8a .. 8a+7 of
+// row w (one 16-byte store), as k_points_ks.
 __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, int C, int64_t n_pad,
                             int R, const uint32_t* __restrict__ slot, int sign_only,
                             uint16_t* __restrict__ vt, Bz bz) {
@@ -170,15 +186,27 @@ __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, in
   vt = zoff(vt, bz.ws);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float s = ldexpf(1.0f, scale_exponent(*slot));
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * R; t += stride) {
-    int64_t blk = t / (32 * (int64_t)R);
-    int rem = (int)(t - blk * 32 * (int64_t)R);
-    int w = rem >> 5;
-    int64_t r = blk * 32 + (rem & 31);
-    float val = (r < n && w < C) ? load_any(v, r * C + w, dtype) * s : 0.0f;
-    if (sign_only) val = (r < n && w == 0) ? (val < 0.0f ? -1.0f : 1.0f) : 0.0f;
-    _Float16 h = (_Float16)val;
-    vt[ks_index(r, w, R)] = __builtin_bit_cast(uint16_t, h);
+  const int64_t total = (n_pad >> 5) * R * 4;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
+    const int a = (int)(t & 3);
+    const int64_t rest = t >> 2;
+    const int64_t blk = rest / R;
+    const int w = (int)(rest - blk * R);
+    uint16_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int z = 8 * a + e;
+      const int64_t r = blk * 32 + 16 * ((z & 7) >> 2) + 4 * (z >> 3) + (z & 3);
+      float val = (r < n && w < C) ? load_any(v, r * C + w, dtype) * s : 0.0f;
+      if (sign_only) val = (r < n && w == 0) ? (val < 0.0f ? -1.0f : 1.0f) : 0.0f;
+      h[e] = __builtin_bit_cast(uint16_t, (_Float16)val);
+    }
+    uint4 pk;
+    pk.x = h[0] | ((uint32_t)h[1] << 16);
+    pk.y = h[2] | ((uint32_t)h[3] << 16);
+    pk.z = h[4] | ((uint32_t)h[5] << 16);
+    pk.w = h[6] | ((uint32_t)h[7] << 16);
+    *reinterpret_cast<uint4*>(vt + ((blk * R + w) * 32 + 8 * a)) = pk;
   }
 }
 
