@@ -224,7 +224,9 @@ def bench_batched(args):
     N, C = v.shape[1], v.shape[2]
     tq, tk, tv = (torch.from_numpy(a).to(dev) for a in (q, k, v))
     # room for every problem in one launch group
-    p_ws = gs.gauss_sum_fwd_batched_workspace_size(M, N, D, C, B, gs.GS_F16, gs.GS_F32)
+    f32 = q.dtype == np.float32
+    qk_code = gs.GS_F32 if f32 else gs.GS_F16
+    p_ws = gs.gauss_sum_fwd_batched_workspace_size(M, N, D, C, B, qk_code, gs.GS_F32)
     ws = torch.empty(max(p_ws, 1), dtype=torch.uint8, device=dev)
     out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
@@ -257,20 +259,26 @@ def bench_batched(args):
     per_launch = float(B) / per_step * M * N * (2 * D + 2 * C)
     avg = float(np.mean(kernel_ms)) if kernel_ms else float("nan")
     achieved = per_launch / (avg * 1e-3) / 1e12
+    # fp32 points: every fp32-accurate product of the scores is three fp16
+    # MFMA products (split operands), so the ceiling of that contraction is a
+    # third of the fp16 peak
+    peak = PEAK_MFMA_F16 / (3.0 if f32 else 1.0)
     res = {
         "metric": METRIC, "value": pairs / (ms_per_step * 1e-3), "unit": "pairs/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "settle": {"ms": settle_ms, "steps": settle_steps},
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f16", "data": "synthetic",
-        "config": {"workload": "%s: B=%d independent clouds, M=N=%d, D=%d, C=%d, f16 points "
-                               "N(0, I/D), tau=1, forward" % (args.workload, B, M, D, C),
+        "dtype": "f32" if f32 else "f16", "data": "synthetic",
+        "config": {"workload": "%s: B=%d independent clouds, M=N=%d, D=%d, C=%d, %s points "
+                               "N(0, I/D), tau=1, forward" % (args.workload, B, M, D, C,
+                                                              "f32" if f32 else "f16"),
                    "B": B, "M": M, "N": N, "D": D, "C": C, "tau": float(tau), "passes": "fwd",
                    "api": "gauss_sum_fwd_batched"},
-        "mfma_frac_of_peak": pairs * (2 * D + 2 * C) / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
-        "roofline": {"bound": "mfma", "kernel": "k_fwd", "achieved": achieved,
-                     "peak": PEAK_MFMA_F16 / 1e12, "unit": "TFLOP/s",
-                     "frac": achieved / (PEAK_MFMA_F16 / 1e12),
-                     "traffic": recorded_traffic(args.workload, "k_fwd"), "avg_launch_ms": avg,
+        "mfma_frac_of_peak": pairs * (2 * D + 2 * C) / (ms_per_step * 1e-3) / peak,
+        "roofline": {"bound": "mfma", "kernel": "k_fwd32" if f32 else "k_fwd", "achieved": achieved,
+                     "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / (peak / 1e12),
+                     "peak_basis": "fp16 MFMA peak / 3 (split fp32 products)" if f32 else "fp16 MFMA peak",
+                     "traffic": recorded_traffic(args.workload, "k_fwd32" if f32 else "k_fwd"),
+                     "avg_launch_ms": avg,
                      "launches": len(kernel_ms), "problems_per_launch": B // per_step,
                      "flops_per_launch": per_launch,
                      "launch_share_of_step": avg * per_step / ms_per_step},
@@ -299,9 +307,11 @@ def compare_attention(args):
     exp(-tau/2 |k|^2), output rescaled by exp(lse - tau/2 |q|^2)) and Alg. 2
     (reweight: queries and keys extended by two entries, one auxiliary key and
     value channel with kappa = sqrt(N + 1), output kappa alpha / beta), both
-    through PyTorch's fused fp16 attention kernels (flash and
-    memory-efficient backends) with q and k shifted by their common mean and
-    the widths padded to multiples of 8 (Sec. 2, Remark 1).  Forward sums of
+    through PyTorch's fused attention kernels (flash and memory-efficient
+    backends) in the points' precision (fp16; fp32 for the single-precision
+    workload, App. A.2, where only the memory-efficient backend takes fp32)
+    with q and k shifted by their common mean and the widths padded to
+    multiples of 8 (Sec. 2, Remark 1).  Forward sums of
     the batched workload; each route is timed like the library (settle,
     warm-up, timed steps between events) and checked against the fp64 oracle
     on sampled rows of three problems (relative L2 error).  Prints one JSON
@@ -323,11 +333,12 @@ def compare_attention(args):
     tq, tk, tv = (torch.from_numpy(a).to(dev) for a in (q, k, v))
     stream = torch.cuda.current_stream()
     ceil8 = lambda x: (x + 7) // 8 * 8
+    pdt = tq.dtype  # the routes compute in the points' precision (fp16, or fp32 for App. A.2)
 
     def centred():
         mu = torch.cat([tq, tk], 1).float().mean(dim=1, keepdim=True)
-        qc = (tq.float() - mu).half()
-        kc = (tk.float() - mu).half()
+        qc = (tq.float() - mu).to(pdt)
+        kc = (tk.float() - mu).to(pdt)
         return qc, kc, qc.float().pow(2).sum(-1), kc.float().pow(2).sum(-1)
 
     def pad(x, width):
@@ -336,7 +347,7 @@ def compare_attention(args):
     def prescale(backend):
         qc, kc, nq, nk = centred()
         w = ceil8(max(D, C))
-        vt = (tv * torch.exp(-0.5 * tau * nk).unsqueeze(-1)).half()
+        vt = (tv * torch.exp(-0.5 * tau * nk).unsqueeze(-1)).to(pdt)
         Q, K, V = (pad(x, w).unsqueeze(1).contiguous() for x in (qc, kc, vt))
         if backend == "flash":
             r = torch.ops.aten._scaled_dot_product_flash_attention(Q, K, V, 0.0, False, False, scale=tau)
@@ -351,16 +362,16 @@ def compare_attention(args):
     def reweight(backend):
         qc, kc, nq, nk = centred()
         w = ceil8(max(D + 2, C + 1))
-        Q = torch.zeros((B, M, w), dtype=torch.float16, device=dev)
+        Q = torch.zeros((B, M, w), dtype=pdt, device=dev)
         Q[..., :D] = qc
         Q[..., D] = 1.0
-        Q[..., D + 1] = (0.5 * nq).half()
-        K = torch.zeros((B, N + 1, w), dtype=torch.float16, device=dev)
+        Q[..., D + 1] = (0.5 * nq).to(pdt)
+        K = torch.zeros((B, N + 1, w), dtype=pdt, device=dev)
         K[:, 0, D + 1] = 1.0
         K[:, 1:, :D] = kc
-        K[:, 1:, D] = (-0.5 * nk).half()
-        V = torch.zeros((B, N + 1, w), dtype=torch.float16, device=dev)
-        V[:, 1:, :C] = tv.half()
+        K[:, 1:, D] = (-0.5 * nk).to(pdt)
+        V = torch.zeros((B, N + 1, w), dtype=pdt, device=dev)
+        V[:, 1:, :C] = tv.to(pdt)
         V[:, 0, C] = kappa
         be = SDPBackend.FLASH_ATTENTION if backend == "flash" else SDPBackend.EFFICIENT_ATTENTION
         with sdpa_kernel([be]):
@@ -425,7 +436,8 @@ def compare_attention(args):
             r["library_speedup"] = r["ms_per_step"] / lib_ms
     print(json.dumps({"mode": "compare_attention", "unit": "pairs/s", "data": "synthetic",
                       "config": {"workload": args.workload, "B": B, "M": M, "N": N, "D": D, "C": C,
-                                 "tau": tau, "passes": "fwd", "inputs": "f16 points, f32 values",
+                                 "tau": tau, "passes": "fwd",
+                                 "inputs": "%s points, f32 values" % ("f32" if pdt == torch.float32 else "f16"),
                                  "accuracy": "rel-L2 vs fp64 oracle, 512 rows of problems %s" % (probs,)},
                       "steps": args.steps, "warmup": args.warmup, "routes": routes}), flush=True)
 
@@ -441,7 +453,7 @@ def main():
                     help="also run a device copy of MIB MiB (counter calibration for --traffic-from)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="record roofline traffic from two rocprofv3 --pmc csv outputs and exit")
-    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32"])
+    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32", "batch_d32_f32"])
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)

@@ -15,6 +15,7 @@
 #include "gs_common.h"
 #include "gs_kernels.h"
 #include "gs_prep.h"
+#include "gs_f32.h"
 
 namespace gs {
 namespace {
@@ -193,6 +194,17 @@ DqK dq_fn(int DP, int CW, int CT, bool fused) {
   return {};
 }
 
+// fp32 tier (fp32 points, C = 1, forward): the kernel for D chunks DP.
+const void* f32_kernel(int DP) {
+  switch (DP) {
+    case 1: return reinterpret_cast<const void*>(&k_fwd32<1>);
+    case 2: return reinterpret_cast<const void*>(&k_fwd32<2>);
+    case 4: return reinterpret_cast<const void*>(&k_fwd32<4>);
+    case 8: return reinterpret_cast<const void*>(&k_fwd32<8>);
+  }
+  return nullptr;
+}
+
 // ------------------------------------------------------------ workspace plan
 
 struct Carver {
@@ -212,6 +224,7 @@ struct Side {  // one point set with the arrays derived from it
   uint16_t* ks = nullptr;       // KS fp16 copy (operand of sum_n P k_n) as keys of a gradient pass
   uint16_t* samp_rt = nullptr;  // kSampleRows sampled rows, RT layout (coarse sample first)
   float* samp_nh = nullptr;     // their half norms
+  uint16_t* lo = nullptr;       // fp32 tier: low fp16 part (rt then holds the high part)
 };
 
 struct Vals {  // one value set (v or dout)
@@ -347,6 +360,24 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   Carver cv;
   cv.base = static_cast<char*>(ws);
   pl.slots = cv.take<uint32_t>(64);
+  if (p.qk_dtype == GS_F32) {
+    // fp32 tier (forward, C = 1): split copies, half norms, step scalars
+    auto split = [&](Side& s, int64_t n_pad) {
+      s.rt = cv.take<uint16_t>(n_pad * W * 2);
+      s.lo = cv.take<uint16_t>(n_pad * W * 2);
+      s.nh = cv.take<float>(n_pad * 4);
+    };
+    split(pl.q, pl.Mp);
+    if (alias)
+      pl.k = pl.q;
+    else
+      split(pl.k, pl.Np);
+    pl.scal_kv = cv.take<float>(pl.Np * 2 * 4);
+    const PassShape ps = pass_shape(p.M, p.N, f32_qt(pl.dm.DP), f32_kernel(pl.dm.DP), G);
+    pl.part = ps.splits > 1 ? cv.take<float>((size_t)ps.splits * p.M * 4) : nullptr;
+    pl.total = cv.off;
+    return;
+  }
   const bool keys_k = w.fwd || w.dq;  // passes whose keys are k
   const bool keys_q = w.dk || w.dv;   // passes whose keys are q
   const bool need_k_ks = w.dq, need_q_ks = w.dk;
@@ -630,6 +661,54 @@ void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t n
   if (fused) combine(c, ps, c.pl->part_s, nq * p.C, out_s, os_s);
 }
 
+// fp32 tier: prep (maxima, split copies, step scalars) and the forward pass
+// of one launch group.  xs / ks / vst / os: byte strides between problems.
+void run_f32(const Ctx& c, const void* q, int64_t qs, const void* k, int64_t ks, const void* v,
+             int64_t vst, float* out, int64_t os) {
+  const gs_problem& p = *c.p;
+  Plan& pl = *c.pl;
+  const int W = pl.dm.W(), DP = pl.dm.DP;
+  const int64_t M = p.M, N = p.N;
+  Bz bz = bz_ws(c);
+  hipLaunchKernelGGL(k_fill_u32, grid_g(c, 1), dim3(64), 0, c.st, pl.slots, 16, 0u, bz);
+  auto points = [&](const void* x, int64_t xs, int64_t n, int64_t n_pad, Side& sd, uint32_t* slot) {
+    Bz b = bz_ws(c);
+    b.in = xs;
+    hipLaunchKernelGGL(k_absmax, grid_g(c, grid_reduce(n * p.D)), dim3(256), 0, c.st, x, n * p.D, 0, slot, b);
+    hipLaunchKernelGGL(k_points_split, grid_g(c, grid1(n_pad * (W / 8))), dim3(256), 0, c.st,
+                       static_cast<const float*>(x), n, (int)p.D, n_pad, W, (const uint32_t*)slot, sd.rt,
+                       sd.lo, sd.nh, b);
+  };
+  points(q, qs, M, pl.Mp, pl.q, pl.slots + 2);
+  if (!pl.alias) points(k, ks, N, pl.Np, pl.k, pl.slots + 3);
+  const int kslot = pl.alias ? 2 : 3;
+  Bz bv = bz_ws(c);
+  bv.in = vst;
+  hipLaunchKernelGGL(k_absmax, grid_g(c, grid_reduce(N)), dim3(256), 0, c.st, v, N, (int)p.v_dtype,
+                     pl.slots + 0, bv);
+  hipLaunchKernelGGL(k_step_scalars32, grid_g(c, grid1(pl.Np * 2)), dim3(256), 0, c.st,
+                     (const float*)pl.k.nh, v, (int)p.v_dtype, N, pl.Np, (const uint32_t*)pl.slots + 0,
+                     (const uint32_t*)pl.slots + 2, (const uint32_t*)pl.slots + kslot, c.tau2, pl.scal_kv, bv);
+  const PassShape ps = pass_shape(M, N, f32_qt(DP), f32_kernel(DP), pl.G);
+  const bool split = ps.splits > 1;
+  float* dst = split ? pl.part : out;
+  Bz bk = bz_ws(c);
+  bk.out = split ? c.slice : os;
+  const dim3 grid = grid_g(c, ps.blocks, ps.splits), block(kBlockThreads);
+  const uint4 *qh = (const uint4*)pl.q.rt, *ql = (const uint4*)pl.q.lo;
+  const uint4 *kh = (const uint4*)pl.k.rt, *kl = (const uint4*)pl.k.lo;
+  const int64_t pst = split ? M : 0;
+  prof_before(kKindFwd, c.st);
+  switch (DP) {
+    case 1: hipLaunchKernelGGL(k_fwd32<1>, grid, block, 0, c.st, qh, ql, (const float*)pl.q.nh, kh, kl, (const float*)pl.scal_kv, (const uint32_t*)pl.slots, kslot, c.tau2, M, ps.steps, ps.sps, dst, pst, bk); break;
+    case 2: hipLaunchKernelGGL(k_fwd32<2>, grid, block, 0, c.st, qh, ql, (const float*)pl.q.nh, kh, kl, (const float*)pl.scal_kv, (const uint32_t*)pl.slots, kslot, c.tau2, M, ps.steps, ps.sps, dst, pst, bk); break;
+    case 4: hipLaunchKernelGGL(k_fwd32<4>, grid, block, 0, c.st, qh, ql, (const float*)pl.q.nh, kh, kl, (const float*)pl.scal_kv, (const uint32_t*)pl.slots, kslot, c.tau2, M, ps.steps, ps.sps, dst, pst, bk); break;
+    case 8: hipLaunchKernelGGL(k_fwd32<8>, grid, block, 0, c.st, qh, ql, (const float*)pl.q.nh, kh, kl, (const float*)pl.scal_kv, (const uint32_t*)pl.slots, kslot, c.tau2, M, ps.steps, ps.sps, dst, pst, bk); break;
+  }
+  prof_after(kKindFwd, c.st);
+  combine(c, ps, pl.part, M, out, os);
+}
+
 void fill_zero(hipStream_t st, float* p, int64_t n) {
   if (p && n > 0) hipLaunchKernelGGL(k_fill_f32, dim3(grid1(n)), dim3(256), 0, st, p, n, 0.0f);
 }
@@ -646,8 +725,15 @@ gs_status check_problem(const gs_problem* p) {
       p->C > GAUSS_SUM_MAX_DIM)
     return GS_ERR_BAD_SHAPE;
   if (p->M > (int64_t(1) << 36) || p->N > (int64_t(1) << 36)) return GS_ERR_BAD_SHAPE;
-  if (p->qk_dtype != GS_F16 && p->qk_dtype != GS_BF16) return GS_ERR_UNSUPPORTED;
+  if (!valid_dtype(p->qk_dtype)) return GS_ERR_UNSUPPORTED;
   if (!valid_dtype(p->v_dtype)) return GS_ERR_UNSUPPORTED;
+  return GS_SUCCESS;
+}
+
+// The fp32 tier (fp32 points) computes the forward sum of a single channel
+// only.
+gs_status check_tier(const gs_problem* p, bool grads) {
+  if (p->qk_dtype == GS_F32 && (grads || p->C != 1)) return GS_ERR_UNSUPPORTED;
   return GS_SUCCESS;
 }
 
@@ -763,6 +849,7 @@ constexpr int64_t kMaxGroup = 65535;
 size_t workspace_for(const gs_problem* p, bool fwd, int want_dq, int want_dk, int want_dv,
                      int64_t count = 1) {
   if (check_problem(p) != GS_SUCCESS) return 0;
+  if (check_tier(p, want_dq || want_dk || want_dv) != GS_SUCCESS) return 0;
   if (p->M == 0 || p->N == 0 || count < 1) return 0;
   Want w = want_for(*p, fwd, want_dq != 0, want_dk != 0, want_dv != 0);
   if (!w.fwd && !w.dq && !w.dk && !w.dv) return 0;
@@ -810,6 +897,8 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
   if ((st = check_tau(tau)) != GS_SUCCESS) return st;
   const int64_t M = p->M, N = p->N, D = p->D, C = p->C;
   const bool grads = dq || dk || dv;
+  if ((st = check_tier(p, grads)) != GS_SUCCESS) return st;
+  const int64_t ps = (int64_t)dsize(p->qk_dtype);  // bytes per point coordinate
   gs_batch one{};
   one.count = 1;
   if (b) {
@@ -830,15 +919,15 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
   const int64_t vs = (int64_t)dsize(p->v_dtype), gsz = (int64_t)dsize(dout_dtype);
   // (strides count elements, so every problem's pointers keep the alignment
   // of the first one's)
-  if ((M > 0 && (!aligned(q, 2) || (grads && !aligned(dout, gsz)))) ||
-      (N > 0 && (!aligned(k, 2) || !aligned(v, vs))) || (out && !aligned(out, 4)) ||
+  if ((M > 0 && (!aligned(q, ps) || (grads && !aligned(dout, gsz)))) ||
+      (N > 0 && (!aligned(k, ps) || !aligned(v, vs))) || (out && !aligned(out, 4)) ||
       (dq && !aligned(dq, 4)) || (dk && !aligned(dk, 4)) || (dv && !aligned(dv, 4)))
     return GS_ERR_MISALIGNED;
   // operand spans over the whole batch
   auto span = [&](const void* base, int64_t stride, int64_t esize, int64_t elems) {
     return range_of(base, base ? ((cnt - 1) * stride + elems) * esize : 0);
   };
-  const Range in[4] = {span(q, bt.q_stride, 2, M * D), span(k, bt.k_stride, 2, N * D),
+  const Range in[4] = {span(q, bt.q_stride, ps, M * D), span(k, bt.k_stride, ps, N * D),
                        span(v, bt.v_stride, vs, N * C),
                        span(grads ? dout : nullptr, bt.dout_stride, gsz, M * C)};
   const Range outs[4] = {span(out, bt.out_stride, 4, out ? M * C : 0),
@@ -871,7 +960,9 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
   // the same array for q and k in every problem
   const bool alias = (q == k) && (M == N) && (cnt == 1 || bt.q_stride == bt.k_stride);
   Want w = want_for(*p, out != nullptr, dq != nullptr, dk != nullptr, dv != nullptr);
-  {
+  if (p->qk_dtype == GS_F32) {
+    if (!f32_kernel(dims_of(D, C).DP)) return GS_ERR_INTERNAL;
+  } else {
     // every kernel the passes below launch must exist for this shape
     const Dims dm = dims_of(D, C);
     if (((w.fwd && !w.fused()) || w.dv) && !fwd_for(*p, dm).launch) return GS_ERR_INTERNAL;
@@ -888,7 +979,7 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
   make_plan(*p, w, alias, workspace, pl, G);
 
   // byte strides between problems
-  const int64_t qs = bt.q_stride * 2, ks = bt.k_stride * 2, vst = bt.v_stride * vs,
+  const int64_t qs = bt.q_stride * ps, ks = bt.k_stride * ps, vst = bt.v_stride * vs,
                 gst = bt.dout_stride * gsz, os = bt.out_stride * 4, dqs = bt.dq_stride * 4,
                 dks = bt.dk_stride * 4, dvs = bt.dv_stride * 4;
   auto at = [](const void* base, int64_t i, int64_t bytes) -> const char* {
@@ -909,6 +1000,10 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
     float* dq_ = at_o(dq, g0, dqs);
     float* dk_ = at_o(dk, g0, dks);
     float* dv_ = at_o(dv, g0, dvs);
+    if (p->qk_dtype == GS_F32) {
+      run_f32(c, q_, qs, k_, ks, v_, vst, out_, os);
+      continue;
+    }
     hipLaunchKernelGGL(k_fill_u32, grid_g(c, 1), dim3(64), 0, stream, pl.slots, 16, 0u, bz_ws(c));
     if (alias) {
       // q.ks serves dk (keys q, signs of dout) unless only dq wants a KS copy
@@ -1009,7 +1104,8 @@ gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, c
 }
 
 size_t gauss_sum_mmd_flow_workspace_size(const gs_problem* p) {
-  if (!p || gs::check_problem(p) != GS_SUCCESS || p->M != p->N || p->C != 1) return 0;
+  if (!p || gs::check_problem(p) != GS_SUCCESS || p->M != p->N || p->C != 1 || p->qk_dtype == GS_F32)
+    return 0;
   return flow_extra(p->N) + gs::workspace_for(p, true, 1, 0, 0);
 }
 
@@ -1022,7 +1118,7 @@ gs_status gauss_sum_mmd_flow(const gs_problem* p, const void* x, const void* v, 
     if (st != GS_SUCCESS) return st;
     if ((st = check_tau(tau)) != GS_SUCCESS) return st;
     if (p->M != p->N) return GS_ERR_BAD_SHAPE;
-    if (p->C != 1) return GS_ERR_UNSUPPORTED;
+    if (p->C != 1 || p->qk_dtype == GS_F32) return GS_ERR_UNSUPPORTED;
     if (!s && !grad && !mmd2) return GS_ERR_NULL_POINTER;
     const int64_t n = p->N, D = p->D;
     if (n > 0 && (!x || !v)) return GS_ERR_NULL_POINTER;

@@ -6,12 +6,16 @@ outputs, workspace) and the stream.  There is no fallback: if the library is
 missing or a call fails, an exception is raised.
 
 Entry points mirror the C names:
-  gauss_sum_fwd(q, k, v, tau)                       -> s        (Eq. 1)
+  gauss_sum_fwd(q, k, v, tau)                       -> s        (Eq. 1; fp32
+                                                       points: the fp32-accuracy
+                                                       tier, C = 1)
   gauss_sum_bwd(q, k, v, tau, dout, want=...)       -> dq, dk, dv
   gauss_sum_fwd_bwd(q, k, v, tau, dout, want=...)   -> s, dq, dk, dv (one call;
                                                        s and dq from one pass)
   gauss_sum_fwd_workspace_size / gauss_sum_bwd_workspace_size /
   gauss_sum_fwd_bwd_workspace_size
+  gauss_sum_fwd_batched / gauss_sum_bwd_batched (B independent problems,
+  grid.z) and their workspace sizes; gauss_sum_mmd_flow (s, flow field, MMD^2)
   gauss_sum_status_string / gauss_sum_abi_version
 and ``GaussSum`` wraps both in a torch.autograd.Function.
 """

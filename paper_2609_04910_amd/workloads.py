@@ -197,26 +197,30 @@ BATCHED = {
     # Sec. 4 benchmark layout: B independent standard Gaussian clouds scaled by
     # D^(-1/2), M = N, tau = 1, fp16 (the D sweep uses B = 64, N = 16384, C = 1)
     "batch_d32": dict(B=64, M=16384, N=16384, D=32, C=1),
+    # the same layout in single precision (App. A.2, the D sweep in fp32)
+    "batch_d32_f32": dict(B=64, M=16384, N=16384, D=32, C=1, qk="f32"),
 }
 
 
 def make_batch(name: str, seed: int = 0, B: Optional[int] = None, M: Optional[int] = None):
     """Batched workload ``name``: (q, k, v, tau) with q, k of shape B x M x D
-    (fp16, N(0, I / D)) and v of shape B x N x C (fp32, N(0, 1)); draws in the
-    order points (q then k, problem by problem), then values."""
+    (fp16, or fp32 where the entry says qk="f32"; N(0, I / D)) and v of shape
+    B x N x C (fp32, N(0, 1)); draws in the order points (q then k, problem by
+    problem), then values."""
     cfg = dict(BATCHED[name])
     if B is not None:
         cfg["B"] = B
     if M is not None:
         cfg["M"] = cfg["N"] = M
     B_, M_, N_, D_, C_ = cfg["B"], cfg["M"], cfg["N"], cfg["D"], cfg["C"]
+    pt = np.float32 if cfg.get("qk") == "f32" else np.float16
     rng = np.random.default_rng(seed)
     s = np.float32(1.0 / np.sqrt(D_))
-    q = np.empty((B_, M_, D_), np.float16)
-    k = np.empty((B_, N_, D_), np.float16)
+    q = np.empty((B_, M_, D_), pt)
+    k = np.empty((B_, N_, D_), pt)
     for b in range(B_):
-        q[b] = (rng.standard_normal((M_, D_), dtype=np.float32) * s).astype(np.float16)
-        k[b] = (rng.standard_normal((N_, D_), dtype=np.float32) * s).astype(np.float16)
+        q[b] = (rng.standard_normal((M_, D_), dtype=np.float32) * s).astype(pt)
+        k[b] = (rng.standard_normal((N_, D_), dtype=np.float32) * s).astype(pt)
     v = rng.standard_normal((B_, N_, C_), dtype=np.float32)
     return q, k, v, np.float32(1.0)
 

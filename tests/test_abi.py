@@ -196,6 +196,26 @@ def test_workspace_sizes():
     assert flow % 256 == 0
 
 
+def test_f32_tier_validation():
+    """fp32 points: the forward of one channel only; everything else is
+    unsupported, and points are aligned to 4 bytes."""
+    lib = gs.load()
+    F = gs.GS_F32
+    assert _fwd(qk=F, C=2) == 4
+    assert _fwd(qk=F, C=1, q=FAKE + 2) == 5
+    assert _fwd(qk=F, C=1, out=FAKE + 0x10000 + 4 * 8 * 4 - 4) == 9  # out meets the k span (fp32 points)
+    assert _bwd(qk=F, C=1) == 4
+    prob = gs.make_problem(8, 8, 4, 1, F, gs.GS_F32)
+    assert lib.gauss_sum_mmd_flow(ctypes.byref(prob), FAKE, FAKE + 0x20000, ctypes.c_float(1.0),
+                                  FAKE + 0x30000, None, None, FAKE + 0x100000, 1 << 40, None) == 4
+    assert gs.gauss_sum_mmd_flow_workspace_size(64, 8, F) == 0
+    assert gs.gauss_sum_bwd_workspace_size(64, 64, 8, 1, F) == 0
+    assert gs.gauss_sum_fwd_workspace_size(64, 64, 8, 2, F) == 0
+    one = gs.gauss_sum_fwd_workspace_size(1000, 3000, 64, 1, F)
+    assert one > 0 and one % 256 == 0
+    assert gs.gauss_sum_fwd_batched_workspace_size(1000, 3000, 64, 1, 1, F) == one
+
+
 def test_batched_workspace_sizes():
     # one problem per group: exactly the single-problem workspace
     assert gs.gauss_sum_fwd_batched_workspace_size(1000, 3000, 64, 4, 1) == \
