@@ -274,7 +274,8 @@ def bench_batched(args):
                    "B": B, "M": M, "N": N, "D": D, "C": C, "tau": float(tau), "passes": "fwd",
                    "api": "gauss_sum_fwd_batched"},
         "mfma_frac_of_peak": pairs * (2 * D + 2 * C) / (ms_per_step * 1e-3) / peak,
-        "roofline": {"bound": "mfma", "kernel": "k_fwd32" if f32 else "k_fwd", "achieved": achieved,
+        "roofline": {"bound": "mfma", "kernel": ("k_fwd32" if C == 1 else "k_fwd32c") if f32 else "k_fwd",
+                     "achieved": achieved,
                      "peak": peak / 1e12, "unit": "TFLOP/s", "frac": achieved / (peak / 1e12),
                      "peak_basis": "fp16 MFMA peak / 3 (split fp32 products)" if f32 else "fp16 MFMA peak",
                      "traffic": recorded_traffic(args.workload, "k_fwd32" if f32 else "k_fwd"),
@@ -388,7 +389,7 @@ def compare_attention(args):
         return out
 
     rows = wl.sample_rows(M, 512, seed=3)
-    probs = (0, B // 2 + 1, B - 1)
+    probs = tuple(sorted({0, B // 2, B - 1}))
     refs = [oracle.fwd(q[b], k[b], v[b], tau, rows=rows, threads=min(oracle.default_threads(), 16))[0]
             for b in probs]
 
@@ -453,7 +454,7 @@ def main():
                     help="also run a device copy of MIB MiB (counter calibration for --traffic-from)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="record roofline traffic from two rocprofv3 --pmc csv outputs and exit")
-    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32", "batch_d32_f32"])
+    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32", "batch_d32_f32", "batch_c32", "batch_c32_f32"])
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)

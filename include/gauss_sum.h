@@ -77,11 +77,11 @@ typedef enum {
 
 /* Problem description.  qk_dtype: GS_F16 or GS_BF16 (both q and k), or
  * GS_F32 for the fp32-accuracy tier (the single-precision setting of App.
- * A.2): the forward sum (gauss_sum_fwd, gauss_sum_fwd_batched) of a single
- * value channel (C == 1), relative error per output about one fp32 ulp of
- * sum_n Phi |v_n| for exponents of order one; every other call, and C > 1,
- * returns GS_ERR_UNSUPPORTED for fp32 points (workspace sizes 0).  Points
- * are aligned to their element size (2 or 4 bytes).
+ * A.2): the forward sum (gauss_sum_fwd, gauss_sum_fwd_batched), error per
+ * output about one fp32 ulp of sum_n Phi |v_nc| for exponents of order one;
+ * the gradient calls and gauss_sum_mmd_flow return GS_ERR_UNSUPPORTED for
+ * fp32 points (workspace sizes 0).  Points are aligned to their element size
+ * (2 or 4 bytes).
  * v_dtype: GS_F32, GS_F16 or GS_BF16. */
 typedef struct {
   int64_t M, N, D, C;

@@ -205,6 +205,62 @@ const void* f32_kernel(int DP) {
   return nullptr;
 }
 
+// fp32 tier, several channels: channel tiles per launch (16 * CT channels)
+// and the launcher of k_fwd32c.
+inline int f32c_ct(int64_t C) {
+  const int64_t cw = std::min<int64_t>(C, kF32MaxChannels);
+  return cw <= 16 ? 1 : cw <= 32 ? 2 : 4;
+}
+
+using F32cFn = void (*)(dim3, hipStream_t, const uint4*, const uint4*, const float*, const uint4*,
+                        const uint4*, const float*, const uint4*, const uint4*, int, const uint32_t*, int,
+                        float, int64_t, int, int, int, int, float*, int64_t, const Bz&);
+
+template <int DP, int CT>
+void launch_f32c(dim3 grid, hipStream_t st, const uint4* qh, const uint4* ql, const float* nhq,
+                 const uint4* kh, const uint4* kl, const float* scal, const uint4* vh, const uint4* vl,
+                 int vstep, const uint32_t* slots, int kslot, float tau2, int64_t M, int C, int cw,
+                 int steps, int sps, float* out, int64_t pstride, const Bz& bz) {
+  hipLaunchKernelGGL((k_fwd32c<DP, CT>), grid, dim3(kBlockThreads), 0, st, qh, ql, nhq, kh, kl, scal, vh,
+                     vl, vstep, slots, kslot, tau2, M, C, cw, steps, sps, out, pstride, bz);
+}
+
+struct F32cK {
+  F32cFn launch = nullptr;
+  const void* kernel = nullptr;
+};
+
+template <int DP, int CT>
+F32cK f32c_k() {
+  return {&launch_f32c<DP, CT>, reinterpret_cast<const void*>(&k_fwd32c<DP, CT>)};
+}
+
+template <int DP>
+F32cK f32c_by_ct(int CT) {
+  switch (CT) {
+    case 1: return f32c_k<DP, 1>();
+    case 2: return f32c_k<DP, 2>();
+    case 4: return f32c_k<DP, 4>();
+  }
+  return {};
+}
+
+F32cK f32c_for(int DP, int CT) {
+  switch (DP) {
+    case 1: return f32c_by_ct<1>(CT);
+    case 2: return f32c_by_ct<2>(CT);
+    case 4: return f32c_by_ct<4>(CT);
+    case 8: return f32c_by_ct<8>(CT);
+  }
+  return {};
+}
+
+// The fp32-tier forward kernel for this shape and its queries per wave.
+const void* f32_pass_kernel(int64_t C, int DP) {
+  return C == 1 ? f32_kernel(DP) : f32c_for(DP, f32c_ct(C)).kernel;
+}
+int f32_pass_qt(int64_t C, int DP) { return C == 1 ? f32_qt(DP) : f32c_qt(DP, f32c_ct(C)); }
+
 // ------------------------------------------------------------ workspace plan
 
 struct Carver {
@@ -361,7 +417,8 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   cv.base = static_cast<char*>(ws);
   pl.slots = cv.take<uint32_t>(64);
   if (p.qk_dtype == GS_F32) {
-    // fp32 tier (forward, C = 1): split copies, half norms, step scalars
+    // fp32 tier (forward): split copies, half norms, step scalars, and for
+    // several channels the split values (KS layout)
     auto split = [&](Side& s, int64_t n_pad) {
       s.rt = cv.take<uint16_t>(n_pad * W * 2);
       s.lo = cv.take<uint16_t>(n_pad * W * 2);
@@ -373,8 +430,12 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
     else
       split(pl.k, pl.Np);
     pl.scal_kv = cv.take<float>(pl.Np * 2 * 4);
-    const PassShape ps = pass_shape(p.M, p.N, f32_qt(pl.dm.DP), f32_kernel(pl.dm.DP), G);
-    pl.part = ps.splits > 1 ? cv.take<float>((size_t)ps.splits * p.M * 4) : nullptr;
+    if (p.C > 1) {
+      pl.v.ks = cv.take<uint16_t>(pl.Np * Rv * 2);  // high parts
+      pl.v.rt = cv.take<uint16_t>(pl.Np * Rv * 2);  // low parts (same KS layout)
+    }
+    const PassShape ps = pass_shape(p.M, p.N, f32_pass_qt(p.C, pl.dm.DP), f32_pass_kernel(p.C, pl.dm.DP), G);
+    pl.part = ps.splits > 1 ? cv.take<float>((size_t)ps.splits * p.M * p.C * 4) : nullptr;
     pl.total = cv.off;
     return;
   }
@@ -684,11 +745,42 @@ void run_f32(const Ctx& c, const void* q, int64_t qs, const void* k, int64_t ks,
   const int kslot = pl.alias ? 2 : 3;
   Bz bv = bz_ws(c);
   bv.in = vst;
-  hipLaunchKernelGGL(k_absmax, grid_g(c, grid_reduce(N)), dim3(256), 0, c.st, v, N, (int)p.v_dtype,
+  const int64_t C = p.C;
+  hipLaunchKernelGGL(k_absmax, grid_g(c, grid_reduce(N * C)), dim3(256), 0, c.st, v, N * C, (int)p.v_dtype,
                      pl.slots + 0, bv);
+  if (C > 1) {
+    const int Rv = pl.dm.Rv();
+    hipLaunchKernelGGL(k_values_ks_split, grid_g(c, grid1(pl.Np / 8 * Rv)), dim3(256), 0, c.st, v,
+                       (int)p.v_dtype, N, (int)C, pl.Np, Rv, (const uint32_t*)pl.slots + 0, pl.v.ks, pl.v.rt,
+                       bv);
+  }
   hipLaunchKernelGGL(k_step_scalars32, grid_g(c, grid1(pl.Np * 2)), dim3(256), 0, c.st,
-                     (const float*)pl.k.nh, v, (int)p.v_dtype, N, pl.Np, (const uint32_t*)pl.slots + 0,
-                     (const uint32_t*)pl.slots + 2, (const uint32_t*)pl.slots + kslot, c.tau2, pl.scal_kv, bv);
+                     (const float*)pl.k.nh, C == 1 ? v : nullptr, (int)p.v_dtype, N, pl.Np,
+                     (const uint32_t*)pl.slots + 0, (const uint32_t*)pl.slots + 2,
+                     (const uint32_t*)pl.slots + kslot, c.tau2, pl.scal_kv, bv);
+  if (C > 1) {
+    // several channels: launches of up to kF32MaxChannels channels each
+    const int CT = f32c_ct(C);
+    const F32cK fk = f32c_for(DP, CT);
+    const PassShape ps = pass_shape(M, N, f32c_qt(DP, CT), fk.kernel, pl.G);
+    const bool split = ps.splits > 1;
+    Bz bk = bz_ws(c);
+    bk.out = split ? c.slice : os;
+    const int Rv = pl.dm.Rv();
+    prof_before(kKindFwd, c.st);
+    for (int64_t c0 = 0; c0 < C; c0 += kF32MaxChannels) {
+      const int cw = (int)std::min<int64_t>(C - c0, kF32MaxChannels);
+      float* dst = (split ? pl.part : out) + c0;
+      fk.launch(grid_g(c, ps.blocks, ps.splits), c.st, (const uint4*)pl.q.rt, (const uint4*)pl.q.lo,
+                (const float*)pl.q.nh, (const uint4*)pl.k.rt, (const uint4*)pl.k.lo, (const float*)pl.scal_kv,
+                (const uint4*)(pl.v.ks + c0 * 32), (const uint4*)(pl.v.rt + c0 * 32), Rv * 64,
+                (const uint32_t*)pl.slots, kslot, c.tau2, M, (int)C, cw, ps.steps, ps.sps, dst,
+                split ? M * C : 0, bk);
+    }
+    prof_after(kKindFwd, c.st);
+    combine(c, ps, pl.part, M * C, out, os);
+    return;
+  }
   const PassShape ps = pass_shape(M, N, f32_qt(DP), f32_kernel(DP), pl.G);
   const bool split = ps.splits > 1;
   float* dst = split ? pl.part : out;
@@ -730,10 +822,9 @@ gs_status check_problem(const gs_problem* p) {
   return GS_SUCCESS;
 }
 
-// The fp32 tier (fp32 points) computes the forward sum of a single channel
-// only.
+// The fp32 tier (fp32 points) computes the forward sum only.
 gs_status check_tier(const gs_problem* p, bool grads) {
-  if (p->qk_dtype == GS_F32 && (grads || p->C != 1)) return GS_ERR_UNSUPPORTED;
+  if (p->qk_dtype == GS_F32 && grads) return GS_ERR_UNSUPPORTED;
   return GS_SUCCESS;
 }
 
@@ -961,7 +1052,7 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
   const bool alias = (q == k) && (M == N) && (cnt == 1 || bt.q_stride == bt.k_stride);
   Want w = want_for(*p, out != nullptr, dq != nullptr, dk != nullptr, dv != nullptr);
   if (p->qk_dtype == GS_F32) {
-    if (!f32_kernel(dims_of(D, C).DP)) return GS_ERR_INTERNAL;
+    if (!f32_pass_kernel(C, dims_of(D, C).DP)) return GS_ERR_INTERNAL;
   } else {
     // every kernel the passes below launch must exist for this shape
     const Dims dm = dims_of(D, C);

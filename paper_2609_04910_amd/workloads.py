@@ -199,6 +199,9 @@ BATCHED = {
     "batch_d32": dict(B=64, M=16384, N=16384, D=32, C=1),
     # the same layout in single precision (App. A.2, the D sweep in fp32)
     "batch_d32_f32": dict(B=64, M=16384, N=16384, D=32, C=1, qk="f32"),
+    # the N sweep with several channels (B = 4, D = C = 32), at N = 16384
+    "batch_c32": dict(B=4, M=16384, N=16384, D=32, C=32),
+    "batch_c32_f32": dict(B=4, M=16384, N=16384, D=32, C=32, qk="f32"),
 }
 
 

@@ -71,7 +71,7 @@ def _bwd(M=8, N=8, D=4, C=2, qk=gs.GS_F16, vd=gs.GS_F32, gd=gs.GS_F32, tau=1.0,
     (dict(C=300), 2), (dict(M=1 << 40), 2),
     (dict(tau=0.0), 3), (dict(tau=-1.0), 3), (dict(tau=float("nan")), 3),
     (dict(tau=float("inf")), 3),
-    (dict(qk=gs.GS_F32), 4), (dict(qk=7), 4), (dict(vd=9), 4),
+    (dict(qk=gs.GS_F32, q=FAKE + 2), 5), (dict(qk=7), 4), (dict(vd=9), 4),
     (dict(q=FAKE + 1), 5), (dict(v=FAKE + 0x20002), 5), (dict(out=FAKE + 0x30002), 5),
     (dict(ws=FAKE + 0x100010), 5),
     (dict(ws=None), 6), (dict(wsb=16), 6),
@@ -197,11 +197,11 @@ def test_workspace_sizes():
 
 
 def test_f32_tier_validation():
-    """fp32 points: the forward of one channel only; everything else is
+    """fp32 points: the forward only (any C); gradients and the flow are
     unsupported, and points are aligned to 4 bytes."""
     lib = gs.load()
     F = gs.GS_F32
-    assert _fwd(qk=F, C=2) == 4
+    assert _fwd(qk=F, C=2, q=FAKE + 2) == 5
     assert _fwd(qk=F, C=1, q=FAKE + 2) == 5
     assert _fwd(qk=F, C=1, out=FAKE + 0x10000 + 4 * 8 * 4 - 4) == 9  # out meets the k span (fp32 points)
     assert _bwd(qk=F, C=1) == 4
@@ -210,7 +210,8 @@ def test_f32_tier_validation():
                                   FAKE + 0x30000, None, None, FAKE + 0x100000, 1 << 40, None) == 4
     assert gs.gauss_sum_mmd_flow_workspace_size(64, 8, F) == 0
     assert gs.gauss_sum_bwd_workspace_size(64, 64, 8, 1, F) == 0
-    assert gs.gauss_sum_fwd_workspace_size(64, 64, 8, 2, F) == 0
+    several = gs.gauss_sum_fwd_workspace_size(1000, 3000, 64, 100, F)
+    assert several > gs.gauss_sum_fwd_workspace_size(1000, 3000, 64, 1, F) and several % 256 == 0
     one = gs.gauss_sum_fwd_workspace_size(1000, 3000, 64, 1, F)
     assert one > 0 and one % 256 == 0
     assert gs.gauss_sum_fwd_batched_workspace_size(1000, 3000, 64, 1, 1, F) == one

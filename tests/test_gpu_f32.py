@@ -1,5 +1,5 @@
-"""GPU parity of the fp32-accuracy tier (fp32 points, C = 1, forward) against
-the fp64 oracle, element by element.
+"""GPU parity of the fp32-accuracy tier (fp32 points, forward; one channel and
+several) against the fp64 oracle, element by element.
 
 Pass rule: |gpu - oracle| <= 1e-5 * A + 1e-30 per element (A = sum_n Phi |v_n|,
 the oracle's scale).  The bound follows from the arithmetic for exponents of
@@ -46,11 +46,11 @@ def _gpu():
     yield
 
 
-def points(seed, M, N, D, spread=1.0, vdt=np.float32):
+def points(seed, M, N, D, spread=1.0, vdt=np.float32, C=1):
     rng = np.random.default_rng(seed)
     q = (spread * rng.standard_normal((M, D))).astype(np.float32)
     k = (spread * rng.standard_normal((N, D))).astype(np.float32)
-    v = rng.standard_normal((N, 1)).astype(vdt)
+    v = rng.standard_normal((N, C)).astype(vdt)
     return q, k, v
 
 
@@ -145,7 +145,7 @@ def test_f32_unsupported_requests_raise():
     with pytest.raises(gs.GaussSumError):
         gs.gauss_sum_bwd(q, q, v, 1.0, torch.randn(10, 1, device="cuda"))
     with pytest.raises(gs.GaussSumError):
-        gs.gauss_sum_fwd(q, q, torch.randn(10, 2, device="cuda"), 1.0)
+        gs.gauss_sum_fwd_bwd(q, q, v, 1.0, torch.randn(10, 1, device="cuda"))
 
 
 def test_f32_benchmark_batch_full_size_sampled_rows():
@@ -176,3 +176,75 @@ def test_f32_positive_values_full_size():
     for b in range(2):
         check("positive[%d]" % b, out[b], q[b], k[b], v[b], float(tau), rows=rows,
               bound=REL_L2_POSITIVE)
+
+
+# (M, N, D, C, tau or None (= 1/D)): channel counts around the 16-row tiles
+# and the 64-channel launches
+SHAPES_C = [
+    (7, 5, 3, 2, None), (65, 129, 17, 15, None), (129, 300, 64, 16, None), (300, 257, 32, 17, None),
+    (517, 700, 40, 32, None), (200, 333, 128, 64, None), (100, 150, 255, 65, None), (96, 200, 16, 100, 0.3),
+    (64, 500, 8, 256, None),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES_C, ids=lambda s: "M%d_N%d_D%d_C%d" % s[:4])
+def test_f32_several_channels_all_outputs(shape):
+    import torch
+    from paper_2609_04910_amd import gauss_sum as gs
+    M, N, D, C, tau = shape
+    tau = np.float32(1.0 / D if tau is None else tau)
+    q, k, v = points(100 + SHAPES_C.index(shape), M, N, D, C=C)
+    out = gs.gauss_sum_fwd(*(torch.from_numpy(a).cuda() for a in (q, k, v)), float(tau))
+    torch.cuda.synchronize()
+    check("f32 %s" % (shape,), out.cpu().numpy(), q, k, v, float(tau), rel_l2=M * N > 1000)
+
+
+def test_f32_several_channels_tiny_kernel_values():
+    """Rows whose kernel values are all far below 1 (sums down to ~1e-20): the
+    exact row-maximum shift keeps full precision; checked relative to A with
+    no absolute floor.  The exponent terms here are far from order one
+    (tau' (||q||^2 + ||k||^2) up to ~190), and the fp32 rounding of the
+    expanded exponent scales with them, so the bound per row is
+    1e-5 * max(1, M_m / 2) with M_m = tau' (||q_m||^2 + max_n ||k_n||^2)."""
+    import torch
+    from paper_2609_04910_amd import gauss_sum as gs
+    q, k, v = points(31, 300, 400, 8, spread=2.0, C=5)
+    tau = 2.0
+    out = gs.gauss_sum_fwd(*(torch.from_numpy(a).cuda() for a in (q, k, v)), tau).cpu().numpy()
+    ref, A = oracle.fwd(q, k, v, tau, threads=parity.oracle_threads())
+    assert 1e-36 < A.min() < 1e-12, (A.min(), A.max())  # rows with tiny sums are present
+    rel = np.abs(out.astype(np.float64) - ref) / A
+    tau2 = tau * np.log2(np.e)
+    mag = tau2 * ((q.astype(np.float64) ** 2).sum(1) + (k.astype(np.float64) ** 2).sum(1).max())
+    bound = TOL32 * np.maximum(1.0, mag / 2)[:, None]
+    _say("  tiny values: A in [%.1e, %.1e], max err/A %.2e, max err/bound %.2f" %
+         (A.min(), A.max(), rel.max(), (rel / bound).max()))
+    assert np.all(rel <= bound)
+
+
+def test_f32_several_channels_positive_and_batched():
+    import torch
+    from paper_2609_04910_amd import gauss_sum as gs
+    q, k, v, tau = wl.make_batch("batch_c32_f32", seed=7, B=3, M=2000)
+    v = np.abs(v)
+    tq, tk, tv = (torch.from_numpy(a).cuda() for a in (q, k, v))
+    a = gs.gauss_sum_fwd_batched(tq, tk, tv, float(tau))
+    b = gs.gauss_sum_fwd_batched(tq, tk, tv, float(tau))
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    for i in range(3):
+        check("c32 positive[%d]" % i, a[i].cpu().numpy(), q[i], k[i], v[i], float(tau),
+              bound=REL_L2_POSITIVE)
+
+
+def test_f32_several_channels_benchmark_batch_full_size():
+    """B = 4 fp32 clouds, N = 16384, D = C = 32 (the paper's single-precision
+    N sweep), all problems in one launch group; sampled rows of two problems."""
+    import torch
+    from paper_2609_04910_amd import gauss_sum as gs
+    q, k, v, tau = wl.make_batch("batch_c32_f32", seed=0)
+    tq, tk, tv = (torch.from_numpy(a).cuda() for a in (q, k, v))
+    out = gs.gauss_sum_fwd_batched(tq, tk, tv, float(tau)).cpu().numpy()
+    rows = wl.sample_rows(q.shape[1], 256, seed=3)
+    for b in (0, 3):
+        check("batch_c32_f32[%d]" % b, out[b], q[b], k[b], v[b], float(tau), rows=rows)
