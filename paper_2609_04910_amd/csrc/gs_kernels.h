@@ -21,23 +21,40 @@
 //
 // Range: kernel values are fp16 numbers in [0, 1].  When every row maximum of
 // the wave's queries over a fixed sample of keys (64 keys; the forward also
-// 1024, via k_row_check) is at least 2^-8 the offset off_m is 0; otherwise
-// the wave first walks its keys once to find the
+// 1024, via k_row_check) is at least 2^-8 the offset off_m is 0.  Otherwise
+// the forward kernel rounds 2^15 Phi instead, the exponent still clamped at
+// <= 0 before the exact shift by 15 (so values are at most 2^15, inside the
+// fp16 range, and keep full relative precision down to Phi = 2^-29), as long
+// as the sampled row maxima are at least 2^-23; below that, and in the
+// gradient kernel below 2^-8, the wave first walks its keys once to find the
 // exact row maximum of the exponent and uses it as off_m (so the largest value
 // of every row is 1 and fp16 keeps full relative precision for all values
-// within 2^-14 of it); the epilogue multiplies by 2^off_m.  Values and
-// upstream gradients are pre-scaled by exact powers of two (largest magnitude
-// in [1, 2)), undone in the epilogue.
+// within 2^-14 of it).  The epilogue multiplies by 2^off_m (off_m = -15 for
+// the shifted rows).  Values and upstream gradients are pre-scaled by exact
+// powers of two (largest magnitude in [1, 2)), undone in the epilogue.
 #pragma once
 
 #include "gs_common.h"
 
+#include <type_traits>
+
 namespace gs {
 
-// Waves whose sampled row maximum of the log2 kernel value falls below this
-// evaluate the row maxima exactly first.
+// Waves whose sampled row maximum of the log2 kernel value falls below
+// kShiftBelow leave the plain [0, 1] range: the forward kernel shifts its
+// kernel values by 2^kSigma (exponent clamped at <= 0 first) while the sampled
+// maxima stay at or above kExactBelow, and evaluates the row maxima exactly
+// below that; the gradient kernel always takes the exact maxima.
 constexpr float kShiftBelow = -8.0f;
+constexpr float kSigma = 15.0f;
+constexpr float kExactBelow = kShiftBelow - kSigma;
 constexpr int kScalarFloats = 64;      // per step: 32 half norms, 32 scaled C = 1 values
+
+// 2^min(y, kSigma): the kernel value times 2^kSigma for y = exponent + kSigma,
+// the exponent clamped at <= 0 (so the result never exceeds 2^kSigma).
+__device__ __forceinline__ float exp2_shifted(float y) {
+  return __builtin_amdgcn_exp2f(fminf(y, kSigma));
+}
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void glb_void;
@@ -185,14 +202,16 @@ __device__ __forceinline__ bool needs_shift(const uint4* __restrict__ sample_rt,
   return __any(low);
 }
 
-// Row-bound check, one flag per query row: shift[m] = 1 when the largest
-// log2 kernel value of row m over the sampled keys (sample_rt / sample_nh: RT
-// layout and half norms, coarse sample first) is below kShiftBelow, i.e. the
-// row needs its exact maximum as offset.  A wave takes 64 rows; it checks the
-// coarse sample first and scans the full one only when some row fails (a
-// clustered key set can hide a row's own cluster from a small sample; the
-// full-sample maximum is never below the coarse one, so rows passing the
-// coarse check pass the full one).  The forward kernel reads these flags.
+// Row-bound check, one flag per query row from the largest log2 kernel value L
+// of row m over the sampled keys (sample_rt / sample_nh: RT layout and half
+// norms, coarse sample first): shift[m] = 0 for L >= kShiftBelow (plain
+// range), 1 for kExactBelow <= L < kShiftBelow (shifted kernel values), 2 below
+// kExactBelow (the row needs its exact maximum as offset).  A wave takes 64
+// rows; it checks the coarse sample first and scans the full one only when
+// some row fails (a clustered key set can hide a row's own cluster from a
+// small sample; the full-sample maximum is never below the coarse one, so rows
+// passing the coarse check pass the full one).  The forward kernel reads these
+// flags.
 template <typename T, int DP>
 __global__ __launch_bounds__(kBlockThreads) void k_row_check(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ sample_rt,
@@ -223,14 +242,15 @@ __global__ __launch_bounds__(kBlockThreads) void k_row_check(
       for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
     }
   };
-  bool low[QT];
+  uint32_t level[QT];
   auto decide = [&]() {
     bool any = false;
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       const float L = fmaf(wave_max_over_g(smax[qt]), tau2, bq[qt]);
-      low[qt] = (q0 + 16 * qt + j < M) && (L < kShiftBelow);
-      any |= low[qt];
+      const bool valid = q0 + 16 * qt + j < M;
+      level[qt] = !valid || L >= kShiftBelow ? 0u : L >= kExactBelow ? 1u : 2u;
+      any |= level[qt] != 0u;
     }
     return __any(any);
   };
@@ -241,7 +261,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_row_check(
   }
   if (g == 0)
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) shift[q0 + 16 * qt + j] = low[qt] ? 1u : 0u;
+    for (int qt = 0; qt < QT; ++qt) shift[q0 + 16 * qt + j] = level[qt];
 }
 
 // The flags of k_row_check for the rows queried against a sample are stored
@@ -250,13 +270,13 @@ __device__ __forceinline__ const uint32_t* row_flags(const float* sample_nh) {
   return reinterpret_cast<const uint32_t*>(sample_nh + kSampleRows);
 }
 
-// Whether any of the wave's 16 QT query rows is flagged by k_row_check.
+// The largest k_row_check level (0, 1, 2) of the wave's 16 QT query rows.
 template <int QT>
-__device__ __forceinline__ bool wave_needs_shift(const uint32_t* __restrict__ shift, int64_t q0, int j) {
+__device__ __forceinline__ int wave_shift_level(const uint32_t* __restrict__ shift, int64_t q0, int j) {
   uint32_t f = 0;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) f |= shift[q0 + 16 * qt + j];
-  return __any(f != 0);
+  for (int qt = 0; qt < QT; ++qt) f = max(f, shift[q0 + 16 * qt + j]);
+  return __any(f >= 2u) ? 2 : __any(f >= 1u) ? 1 : 0;
 }
 
 // Exact row maxima of S~ over the wave's key range, from the RT key copy in
@@ -373,9 +393,21 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     bq[qt] = tau2 * nhq[q0 + 16 * qt + j];
     off[qt] = 0.0f;
   }
-  if (needs_shift<T, DP, QT>(samp_rt, samp_nh, qreg, bq, tau2, q0, M, j, g) &&
-      wave_needs_shift<QT>(row_flags(samp_nh), q0, j))
+  // range of the wave's kernel values: plain [0, 1], shifted by 2^kSigma, or
+  // exact row maxima as offsets (levels of k_row_check)
+  const int level = needs_shift<T, DP, QT>(samp_rt, samp_nh, qreg, bq, tau2, q0, M, j, g)
+                        ? wave_shift_level<QT>(row_flags(samp_nh), q0, j)
+                        : 0;
+  if (level == 2) {
     exact_offsets<T, DP, QT>(ks, scal, qreg, s_begin, s_end, j, g, tau2, bq, off);
+  } else if (level == 1) {
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      off[qt] = -kSigma;
+      bq[qt] += kSigma;
+    }
+  }
+  const bool shifted = level == 1;
 
   floatx4 O[QT][CT];
 #pragma unroll
@@ -383,7 +415,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) O[qt][ct] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  auto compute = [&](int stage) {
+  // one key loop per range mode, so that each keeps the register budget of
+  // a single loop body
+  auto compute = [&](int stage, auto shift_c) {
+    constexpr bool SH = decltype(shift_c)::value;
     const char* base = lds + stage * STAGE;
     const uint4* kb = reinterpret_cast<const uint4*>(base);
     const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
@@ -405,14 +440,20 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
       for (int kt = 0; kt < 2; ++kt) {
         const floatx4 acc = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[r], tau2, bq[qt]));
+        for (int r = 0; r < 4; ++r) {
+          const float y = fmaf(acc[r], tau2, bq[qt]);
+          p[kt][r] = SH ? exp2_shifted(y) : exp2_clamped(y);
+        }
       }
       const uint4 b = pack_tile_pair(p);
 #pragma unroll
       for (int ct = 0; ct < CT; ++ct) O[qt][ct] = mfma_f16(vr[ct], b, O[qt][ct]);
     }
   };
-  key_stream<NS, NCH + 1>(s_begin, s_end, issue, compute);
+  if (shifted)
+    key_stream<NS, NCH + 1>(s_begin, s_end, issue, [&](int st) { compute(st, std::true_type{}); });
+  else
+    key_stream<NS, NCH + 1>(s_begin, s_end, issue, [&](int st) { compute(st, std::false_type{}); });
 
   const int ev = scale_exponent(*vslot) - (ONE ? 1 : 0);
 #pragma unroll
@@ -579,6 +620,35 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
     const uint4* fb = reinterpret_cast<const uint4*>(base + (KCH + VCH + TCH) * 1024);
 #pragma unroll
     for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + j) * 4 + g];
+    if constexpr (CW == 0) {
+      // single channel: the score MFMAs of all query tiles, then their
+      // exponentials, then the contractions over keys and the row sums, kept
+      // apart by scheduling barriers (2 % faster than tile by tile)
+      floatx4 acc[QT][2];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) acc[qt][kt] = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
+      __builtin_amdgcn_sched_barrier(0);
+      uint4 b[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        float p[2][4];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[qt][kt][r], tau2, bq[qt]));
+        b[qt] = pack_tile_pair(p);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) dQ[qt][dt] = mfma_f16(ktr[dt], b[qt], dQ[qt][dt]);
+        rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
+      }
+      return;
+    }
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       float p[2][4], phi[2][4];

@@ -183,6 +183,42 @@ def test_workload_full_size_sampled_rows(name):
         _say("  stats", stats)
 
 
+def test_range_levels_plain_shifted_exact():
+    """Query blocks at growing distance from a key cloud, so that the largest
+    kernel value of a row is about 2^-4 (plain [0, 1] values), 2^-14 and 2^-19
+    (values shifted by 2^15 before rounding to fp16) and 2^-30 (exact row
+    maxima as offsets): every pass matches the oracle in each regime."""
+    import parity
+    rng = np.random.default_rng(5)
+    D, N, C, B = 16, 1500, 3, 512
+    k32 = (0.3 * rng.standard_normal((N, D))).astype(np.float32)
+    targets = (-4.0, -14.0, -19.0, -30.0)   # log2 of the row maximum
+    tau = np.float32(1.0)
+    c = float(tau) * np.log2(np.e) / 2.0     # -log2 Phi = c d^2
+    blocks = []
+    for L in targets:
+        u = rng.standard_normal((B, D))
+        u /= np.linalg.norm(u, axis=1, keepdims=True)
+        # radius with nearest-key squared distance about -L / c
+        proj = np.max(u @ k32.T.astype(np.float64), axis=1)
+        r = np.sqrt(-L / c) + proj
+        blocks.append((u * r[:, None] + 0.02 * rng.standard_normal((B, D))).astype(np.float32))
+    q = np.concatenate(blocks).astype(np.float16)
+    k = k32.astype(np.float16)
+    d2 = ((q.astype(np.float64)[:, None, :] - k.astype(np.float64)[None, :, :]) ** 2).sum(-1)
+    Lrow = -c * d2.min(axis=1)
+    for i, L in enumerate(targets):
+        got = Lrow[i * B:(i + 1) * B]
+        _say("block", i, "target", L, "row max log2 range", float(got.min()), float(got.max()))
+    assert np.all(Lrow[:B] > -8) and np.all(Lrow[B:3 * B] < -8) and np.all(Lrow[B:3 * B] > -23)
+    assert np.all(Lrow[3 * B:] < -23)
+    v = rng.standard_normal((N, C)).astype(np.float32)
+    g = rng.standard_normal((4 * B, C)).astype(np.float32)
+    w = wl.Workload("range_levels", 4 * B, N, D, C, tau, "f16", q, k, v, g,
+                    ("fwd", "dq", "dk", "dv"), False, q, k)
+    _say("  stats", parity.check_workload(w))
+
+
 def test_mixture_tau10_adversarial_rows():
     """The 64 queries with the smallest sum of kernel values (found on the GPU
     with v = 1) are the hardest for fp16 kernel values; check them exactly."""
