@@ -398,9 +398,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
   const int level = needs_shift<T, DP, QT>(samp_rt, samp_nh, qreg, bq, tau2, q0, M, j, g)
                         ? wave_shift_level<QT>(row_flags(samp_nh), q0, j)
                         : 0;
-  if (level == 2) {
-    exact_offsets<T, DP, QT>(ks, scal, qreg, s_begin, s_end, j, g, tau2, bq, off);
-  } else if (level == 1) {
+  if (level == 1) {
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       off[qt] = -kSigma;
@@ -408,6 +406,45 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     }
   }
   const bool shifted = level == 1;
+  if (__syncthreads_or(level == 2)) {
+    // exact row maxima: the workgroup streams its key range once more through
+    // the LDS ring (keys and step scalars only); waves that need no offsets
+    // only take part in the copies and barriers
+    float smax[QT];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) smax[qt] = -__builtin_inff();
+    auto issue_k = [&](int s, int stage) {
+      if (!mine) return;
+      const uint32_t base = lds0 + stage * STAGE;
+      const uint32_t ls = (uint32_t)(s - s_begin);
+#pragma unroll
+      for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+      dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
+    };
+    key_stream<NS, KCH + 1>(s_begin, s_end, issue_k, [&](int stage) {
+      if (level != 2) return;
+      const char* base = lds + stage * STAGE;
+      const uint4* kb = reinterpret_cast<const uint4*>(base);
+      const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const floatx4 cin = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
+        uint4 kr[DP];
+        load_k_tile<DP>(kb, kt, j, g, kr);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
+      }
+    });
+    __syncthreads();  // every wave is done with the ring before the main stream refills it
+    if (level == 2) {
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        off[qt] = fmaf(wave_max_over_g(smax[qt]), tau2, bq[qt]);
+        if (!(off[qt] > -__builtin_inff())) off[qt] = 0.0f;  // empty key range
+        bq[qt] -= off[qt];
+      }
+    }
+  }
 
   floatx4 O[QT][CT];
 #pragma unroll
