@@ -23,6 +23,12 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kMinStepsPerSplit = 4;     // 128 keys
 constexpr int kSplitOverheadSteps = 8;   // per-workgroup fixed cost (prologue, epilogue), in key steps
+// Most key steps one split may cover: every key-side stream moves at most
+// 16 KiB per step, and a split's part of a stream is addressed through one
+// buffer resource (32-bit byte count) with 32-bit step offsets.
+constexpr int kMaxStepsPerSplit = 1 << 17;
+// Largest M and N accepted (key steps and row tiles stay within int).
+constexpr int64_t kMaxRows = int64_t(1) << 35;
 constexpr int kDefaultSlots = 512;       // resident workgroups assumed when no device can be queried
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -348,8 +354,9 @@ PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel, int
   const int64_t slots = device_slots(kernel);
   const int64_t wide = (int64_t)std::max(1, ps.blocks) * std::max<int64_t>(1, group);
   const int cap = std::max(1, ps.steps / kMinStepsPerSplit);
-  const int lo = (int)std::min<int64_t>(cap, std::max<int64_t>(1, ceil_div(slots, wide)));
-  const int hi = std::min(cap, 4 * lo);
+  const int need = (int)std::max<int64_t>(1, ceil_div(ps.steps, kMaxStepsPerSplit));
+  const int lo = std::max(need, (int)std::min<int64_t>(cap, std::max<int64_t>(1, ceil_div(slots, wide))));
+  const int hi = std::max(lo, std::min(cap, 4 * lo));
   auto cost = [&](int sp) {
     return ceil_div(wide * sp, slots) * (ceil_div(ps.steps, sp) + kSplitOverheadSteps);
   };
@@ -816,7 +823,7 @@ gs_status check_problem(const gs_problem* p) {
   if (p->M < 0 || p->N < 0 || p->D < 1 || p->D > GAUSS_SUM_MAX_DIM || p->C < 1 ||
       p->C > GAUSS_SUM_MAX_DIM)
     return GS_ERR_BAD_SHAPE;
-  if (p->M > (int64_t(1) << 36) || p->N > (int64_t(1) << 36)) return GS_ERR_BAD_SHAPE;
+  if (p->M > kMaxRows || p->N > kMaxRows) return GS_ERR_BAD_SHAPE;
   if (!valid_dtype(p->qk_dtype)) return GS_ERR_UNSUPPORTED;
   if (!valid_dtype(p->v_dtype)) return GS_ERR_UNSUPPORTED;
   return GS_SUCCESS;

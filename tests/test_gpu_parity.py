@@ -219,6 +219,41 @@ def test_range_levels_plain_shifted_exact():
     _say("  stats", parity.check_workload(w))
 
 
+def test_many_keys_split_limit():
+    """2^23 + 100 keys at D = 256 with enough query rows that one key split
+    would fill the GPU: the planner must still split the keys so that no
+    split's part of a key stream exceeds what one buffer resource addresses
+    (4 GiB).  Every query has about 64 near copies among the keys, spread
+    over the whole key range, which dominate its sum (tau = 16, positive
+    values), so a key tile read as zeros anywhere changes the result; sampled
+    rows against all keys match the oracle."""
+    import torch
+    import oracle
+    import parity
+    from paper_2609_04910_amd import gauss_sum as gs
+    M, N, D, C = 131072, (1 << 23) + 100, 256, 16
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    q32 = torch.randn(M, D, device="cuda", generator=gen)
+    q32 /= q32.norm(dim=1, keepdim=True)
+    idx = torch.randint(0, M, (N,), device="cuda", generator=gen)
+    k = q32[idx] + 0.01 * torch.randn(N, D, device="cuda", generator=gen)
+    del idx
+    k = (k / k.norm(dim=1, keepdim=True)).half()
+    q = q32.half()
+    del q32
+    v = torch.rand(N, C, device="cuda", generator=gen) + 0.1
+    tau = 16.0
+    s = gs.gauss_sum_fwd(q, k, v, tau)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 4097, M // 2 + 3, M - 1])
+    qh = q[torch.from_numpy(rows).cuda()].cpu().numpy()
+    kh, vh = k.cpu().numpy(), v.cpu().numpy()
+    del k, v
+    ref, scale = oracle.fwd(qh, kh, vh, tau, threads=parity.oracle_threads())
+    got = s[torch.from_numpy(rows).cuda()].cpu().numpy()
+    _say("many keys: row sums", ref[:, 0], parity.compare("many_keys", got, ref, scale, parity.TOL["f16"]))
+
+
 def test_mixture_tau10_adversarial_rows():
     """The 64 queries with the smallest sum of kernel values (found on the GPU
     with v = 1) are the hardest for fp16 kernel values; check them exactly."""
