@@ -65,7 +65,7 @@ typedef enum { GS_F32 = 0, GS_F16 = 1, GS_BF16 = 2 } gs_dtype;
 typedef enum {
   GS_SUCCESS = 0,
   GS_ERR_NULL_POINTER = 1, /* a required pointer is NULL, or no output requested */
-  GS_ERR_BAD_SHAPE = 2,    /* M or N outside [0, 2^35], D or C outside [1, 256] */
+  GS_ERR_BAD_SHAPE = 2,    /* M or N outside [0, 2^30], D or C outside [1, 256] */
   GS_ERR_BAD_TAU = 3,      /* tau not finite or not > 0 (Eq. 1 needs tau > 0) */
   GS_ERR_UNSUPPORTED = 4,  /* dtype combination not supported */
   GS_ERR_MISALIGNED = 5,   /* pointer not aligned as documented above */

@@ -27,8 +27,10 @@ constexpr int kSplitOverheadSteps = 8;   // per-workgroup fixed cost (prologue, 
 // 16 KiB per step, and a split's part of a stream is addressed through one
 // buffer resource (32-bit byte count) with 32-bit step offsets.
 constexpr int kMaxStepsPerSplit = 1 << 17;
-// Largest M and N accepted (key steps and row tiles stay within int).
-constexpr int64_t kMaxRows = int64_t(1) << 35;
+// Largest M and N accepted: the main kernels launch one workgroup of 256
+// threads per 64 QT rows, and a grid's x extent in threads must stay below
+// 2^32 (QT >= 1).
+constexpr int64_t kMaxRows = int64_t(1) << 30;
 constexpr int kDefaultSlots = 512;       // resident workgroups assumed when no device can be queried
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }

@@ -68,7 +68,7 @@ def _bwd(M=8, N=8, D=4, C=2, qk=gs.GS_F16, vd=gs.GS_F32, gd=gs.GS_F32, tau=1.0,
     (dict(p=False), 1),
     (dict(q=None), 1), (dict(k=None), 1), (dict(v=None), 1), (dict(out=None), 1),
     (dict(M=-1), 2), (dict(N=-3), 2), (dict(D=0), 2), (dict(D=257), 2), (dict(C=0), 2),
-    (dict(C=300), 2), (dict(M=1 << 40), 2),
+    (dict(C=300), 2), (dict(M=1 << 40), 2), (dict(M=(1 << 30) + 1), 2), (dict(N=(1 << 30) + 1), 2),
     (dict(tau=0.0), 3), (dict(tau=-1.0), 3), (dict(tau=float("nan")), 3),
     (dict(tau=float("inf")), 3),
     (dict(qk=gs.GS_F32, q=FAKE + 2), 5), (dict(qk=7), 4), (dict(vd=9), 4),
