@@ -301,6 +301,230 @@ def bench_batched(args):
     print(json.dumps(res), flush=True)
 
 
+def bench_batched_grad(args):
+    """Batched forward plus backward (the paper's forward-and-backward
+    benchmark layout, Sec. 4): one gauss_sum_fwd_bwd_batched call per step
+    over B independent clouds giving s and dq, dk, dv for an upstream gradient
+    dout; pairs/s counts B M N per step."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2609_04910_amd import gauss_sum as gs
+    from paper_2609_04910_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    q, k, v, tau = wl.make_batch(args.workload, seed=0)
+    g = wl.batch_dout(args.workload, seed=0)
+    B, M, D = q.shape
+    N, C = v.shape[1], v.shape[2]
+    tq, tk, tv, tg = (torch.from_numpy(a).to(dev) for a in (q, k, v, g))
+    ws = torch.empty(max(gs.gauss_sum_fwd_bwd_batched_workspace_size(M, N, D, C, B), 1),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gs.gauss_sum_fwd_bwd_batched(tq, tk, tv, float(tau), tg, out=out, workspace=ws, stream=stream)
+
+    settle_steps, t0 = 0, time.perf_counter()
+    while settle_steps == 0 or (time.perf_counter() - t0) * 1e3 < args.settle_ms:
+        step()
+        settle_steps += 1
+        torch.cuda.synchronize()
+    settle_ms = (time.perf_counter() - t0) * 1e3
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    cap = args.steps * 4
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    gs.gauss_sum_profile_start(cap, gs.PROFILE_GRAD)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    kernel_ms = gs.gauss_sum_profile_stop(cap)
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    pairs = float(B) * M * N
+    # gradient-kind launches per step: the dq pass (forward fused) and the dk pass
+    per_step = max(1, len(kernel_ms) // args.steps)
+    grad_ms = float(np.sum(kernel_ms)) / args.steps if kernel_ms else float("nan")
+    # algorithmic flops of one step: the dq pass with the forward fused 4D+4C,
+    # the dk pass 4D+2C, the dv pass 2D+2C per pair
+    flops = pairs * ((4 * D + 4 * C) + (4 * D + 2 * C) + (2 * D + 2 * C))
+    grad_flops = pairs * ((4 * D + 4 * C) + (4 * D + 2 * C))
+    res = {
+        "metric": METRIC, "value": pairs / (ms_per_step * 1e-3), "unit": "pairs/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "settle": {"ms": settle_ms, "steps": settle_steps},
+        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+        "config": {"workload": "%s: B=%d independent clouds, M=N=%d, D=%d, C=%d, f16 points N(0, I/D), "
+                               "tau=1, forward and gradients w.r.t. q, k, v" % (args.workload, B, M, D, C),
+                   "B": B, "M": M, "N": N, "D": D, "C": C, "tau": float(tau), "passes": "fwd+dq+dk+dv",
+                   "api": "gauss_sum_fwd_bwd_batched"},
+        "mfma_frac_of_peak": flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
+        "roofline": {"bound": "mfma", "kernel": "k_dq (dq pass with the forward fused, and dk pass)",
+                     "achieved": grad_flops / (grad_ms * 1e-3) / 1e12, "peak": PEAK_MFMA_F16 / 1e12,
+                     "unit": "TFLOP/s",
+                     "frac": grad_flops / (grad_ms * 1e-3) / PEAK_MFMA_F16,
+                     "traffic": None, "avg_launch_ms": grad_ms / per_step, "launches": len(kernel_ms),
+                     "launches_per_step": per_step, "flops_per_step": grad_flops,
+                     "launch_share_of_step": grad_ms / ms_per_step},
+    }
+    if not args.no_cpu:
+        threads = min(oracle.default_threads(), 16)
+        rows = wl.sample_rows(M, 64, seed=5)
+        oracle.dq(q[0], k[0], v[0], g[0], float(tau), rows=rows[:1], threads=threads)
+        t0, done = time.perf_counter(), 0
+        while done == 0 or time.perf_counter() - t0 < args.cpu_budget:
+            b = done % B
+            oracle.fwd(q[b], k[b], v[b], float(tau), rows=rows, threads=threads)
+            oracle.dq(q[b], k[b], v[b], g[b], float(tau), rows=rows, threads=threads)
+            oracle.dk(q[b], k[b], v[b], g[b], float(tau), rows=rows, threads=threads)
+            oracle.dv(q[b], k[b], v[b], g[b], float(tau), rows=rows, threads=threads)
+            done += 1
+        t = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": done * len(rows) * float(N) / t, "unit": "pairs/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": "fp64 oracle, forward, dq, dk and dv on %d sampled rows of a "
+                                         "problem (each against all %d partners), %d problems, %.1f s"
+                                         % (len(rows), N, done, t)}
+    print(json.dumps(res), flush=True)
+
+
+def compare_attention_grad(args):
+    """The paper's gradient route on this GPU, as an external comparison (not
+    part of the library): Alg. 2 (reweight) through PyTorch's public
+    scaled_dot_product_attention with automatic differentiation, the backward
+    pass again in the fused attention kernels (Sec. 2, Remark 1; Alg. 1 needs
+    the log-sum-exp output, which the attention backward does not
+    differentiate), for s and the gradients of sum(dout * s) with respect to
+    q, k and v in fp16, beside one gauss_sum_fwd_bwd_batched call.  Each route
+    is timed like the library and checked against the fp64 oracle on sampled
+    rows of three problems (relative L2 error of s and of dq).  Prints one
+    JSON line."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    import oracle
+    from paper_2609_04910_amd import gauss_sum as gs
+    from paper_2609_04910_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    q, k, v, tau = wl.make_batch(args.workload, seed=0, M=args.batch_n)
+    g = wl.batch_dout(args.workload, seed=0, M=args.batch_n)
+    tau = float(tau)
+    B, M, D = q.shape
+    N, C = v.shape[1], v.shape[2]
+    tq, tk, tv, tg = (torch.from_numpy(a).to(dev) for a in (q, k, v, g))
+    stream = torch.cuda.current_stream()
+    ceil8 = lambda x: (x + 7) // 8 * 8
+    kappa = float(np.sqrt(N + 1))
+    lq = tq.clone().requires_grad_(True)
+    lk = tk.clone().requires_grad_(True)
+    lv = tv.clone().requires_grad_(True)
+
+    def reweight(backend):
+        for t in (lq, lk, lv):
+            t.grad = None
+        mu = torch.cat([lq, lk], 1).float().mean(dim=1, keepdim=True)
+        qc = (lq.float() - mu).half()
+        kc = (lk.float() - mu).half()
+        nq, nk = qc.float().pow(2).sum(-1), kc.float().pow(2).sum(-1)
+        w = ceil8(max(D + 2, C + 1))
+        Q = torch.zeros((B, M, w), dtype=torch.float16, device=dev)
+        Q[..., :D] = qc
+        Q[..., D] = 1.0
+        Q[..., D + 1] = (0.5 * nq).half()
+        K = torch.zeros((B, N + 1, w), dtype=torch.float16, device=dev)
+        K[:, 0, D + 1] = 1.0
+        K[:, 1:, :D] = kc
+        K[:, 1:, D] = (-0.5 * nk).half()
+        V = torch.zeros((B, N + 1, w), dtype=torch.float16, device=dev)
+        V[:, 1:, :C] = lv.half()
+        V[:, 0, C] = kappa
+        be = SDPBackend.FLASH_ATTENTION if backend == "flash" else SDPBackend.EFFICIENT_ATTENTION
+        with sdpa_kernel([be]):
+            o = F.scaled_dot_product_attention(Q.unsqueeze(1), K.unsqueeze(1), V.unsqueeze(1), scale=tau)
+        o = o[:, 0].float()
+        s = kappa * o[..., :C] / o[..., C:C + 1]
+        (s * tg).sum().backward()
+        return s.detach(), lq.grad
+
+    ws = torch.empty(max(gs.gauss_sum_fwd_bwd_batched_workspace_size(M, N, D, C, B), 1),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
+
+    def library():
+        s, dq, _, _ = gs.gauss_sum_fwd_bwd_batched(tq, tk, tv, tau, tg, out=out, workspace=ws,
+                                                   stream=stream)
+        return s, dq
+
+    rows = wl.sample_rows(M, 256, seed=3)
+    probs = tuple(sorted({0, B // 2, B - 1}))
+    th = min(oracle.default_threads(), 16)
+    ref_s = [oracle.fwd(q[b], k[b], v[b], tau, rows=rows, threads=th)[0] for b in probs]
+    ref_dq = [oracle.dq(q[b], k[b], v[b], g[b], tau, rows=rows, threads=th)[0] for b in probs]
+
+    def rel(got, refs):
+        num = sum(float(np.sum((got[b][rows].astype(np.float64) - r) ** 2)) for b, r in zip(probs, refs))
+        den = sum(float(np.sum(r ** 2)) for r in refs)
+        return float(np.sqrt(num / den))
+
+    def measure(fn):
+        s, dq = fn()
+        torch.cuda.synchronize()
+        sh, dqh = s.float().cpu().numpy(), dq.float().cpu().numpy()
+        acc = {}
+        for key, got, refs in (("s", sh, ref_s), ("dq", dqh, ref_dq)):
+            bad = float(np.mean(~np.isfinite(got)))
+            acc["nonfinite_" + key] = bad   # fraction of non-finite outputs (fp16 overflow)
+            acc["rel_l2_" + key] = rel(got, refs) if bad == 0.0 else None
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < args.settle_ms:
+            fn()
+            torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        return dict(ms_per_step=ms, pairs_per_s=B * float(M) * N / (ms * 1e-3), **acc)
+
+    routes = {}
+    for name, fn in (("gauss_sum_fwd_bwd_batched", library),
+                     ("alg2_reweight_flash_autograd", lambda: reweight("flash")),
+                     ("alg2_reweight_mem_efficient_autograd", lambda: reweight("efficient"))):
+        print("route", name, flush=True, file=sys.stderr)
+        try:
+            torch.cuda.reset_peak_memory_stats()
+            base = torch.cuda.memory_allocated()
+            routes[name] = measure(fn)
+            routes[name]["peak_mem_gib"] = (torch.cuda.max_memory_allocated() - base) / 2 ** 30
+        except RuntimeError as e:  # a backend that does not take these shapes here
+            routes[name] = {"error": str(e).splitlines()[0][:200]}
+    lib_ms = routes["gauss_sum_fwd_bwd_batched"]["ms_per_step"]
+    for r in routes.values():
+        if "ms_per_step" in r:
+            r["library_speedup"] = r["ms_per_step"] / lib_ms
+    print(json.dumps({"mode": "compare_attention", "unit": "pairs/s", "data": "synthetic",
+                      "config": {"workload": args.workload, "B": B, "M": M, "N": N, "D": D, "C": C,
+                                 "tau": tau, "passes": "fwd+dq+dk+dv", "inputs": "f16 points, f32 values",
+                                 "accuracy": "rel-L2 of s and dq vs fp64 oracle, %d rows of problems %s"
+                                             % (len(rows), probs)},
+                      "steps": args.steps, "warmup": args.warmup, "routes": routes}), flush=True)
+
+
 def compare_attention(args):
     """The paper's route on this GPU, as an external comparison (it is not part
     of the library and nothing in the library calls it): Alg. 1 (prescale:
@@ -454,7 +678,7 @@ def main():
                     help="also run a device copy of MIB MiB (counter calibration for --traffic-from)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="record roofline traffic from two rocprofv3 --pmc csv outputs and exit")
-    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32", "batch_d32_f32", "batch_c32", "batch_c32_f32"])
+    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32", "batch_d32_f32", "batch_c32", "batch_c32_f32", "batch_grad_d32"])
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -463,7 +687,10 @@ def main():
                          "and MMD^2 = v^T s) instead of gauss_sum_fwd_bwd")
     ap.add_argument("--compare-attention", action="store_true",
                     help="batched workloads: time the paper's attention route (Alg. 1 and 2 through "
-                         "PyTorch's fused attention) beside the library, forward only")
+                         "PyTorch's fused attention; for batch_grad_d32 forward and backward through "
+                         "Alg. 2 with autograd) beside the library")
+    ap.add_argument("--batch-n", type=int, default=None, metavar="N",
+                    help="--compare-attention on batch_grad_d32: M = N = this instead of 65536")
     ap.add_argument("--separate", action="store_true",
                     help="time separate gauss_sum_fwd + gauss_sum_bwd calls instead of one "
                          "gauss_sum_fwd_bwd call")
@@ -495,10 +722,16 @@ def main():
         if args.workload not in wl.BATCHED:
             print("--compare-attention takes a batched workload (--workload batch_d32)", file=sys.stderr)
             sys.exit(2)
-        compare_attention(args)
+        if wl.BATCHED[args.workload].get("grad"):
+            compare_attention_grad(args)
+        else:
+            compare_attention(args)
         return
     if args.workload in wl.BATCHED:
-        bench_batched(args)
+        if wl.BATCHED[args.workload].get("grad"):
+            bench_batched_grad(args)
+        else:
+            bench_batched(args)
         return
 
     passes = PASSES[args.workload]

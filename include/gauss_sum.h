@@ -180,6 +180,21 @@ gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, cons
 size_t gauss_sum_bwd_batched_workspace_size(const gs_problem* p, int64_t count, int want_dq,
                                             int want_dk, int want_dv);
 
+/* gauss_sum_fwd_bwd for each problem of the batch (as gauss_sum_fwd_batched;
+ * the forward sum rides along in the dq pass where gauss_sum_fwd_bwd fuses
+ * it; one slice is gauss_sum_fwd_bwd_workspace_size(p, ...) bytes).  This is
+ * the layout of the paper's forward-plus-backward benchmark (Sec. 4, the
+ * N sweep with B = 4 clouds). */
+gs_status gauss_sum_fwd_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
+                                    const void* k, const void* v, float tau, const void* dout,
+                                    gs_dtype dout_dtype, float* out, float* dq, float* dk, float* dv,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes for gauss_sum_fwd_bwd_batched to run `count` problems in
+ * one launch group (as gauss_sum_fwd_batched_workspace_size). */
+size_t gauss_sum_fwd_bwd_batched_workspace_size(const gs_problem* p, int64_t count, int want_dq,
+                                                int want_dk, int want_dv);
+
 /* One MMD-flow evaluation (Sec. 3, the MMD and particle-flow paragraphs):
  * points x (N x D, qk_dtype) serve as both queries and keys, v (N x 1,
  * v_dtype) are the signed weights of sigma = mu - nu = sum_n v_n delta_{x_n}.

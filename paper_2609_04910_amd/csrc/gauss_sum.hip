@@ -388,6 +388,9 @@ struct Want {
   bool fwd = false, dq = false, dk = false, dv = false;
   bool fuse = false;  // set by want_for (kFuseMaxC, kFuseMaxD)
   bool fused() const { return fwd && dq && fuse; }  // forward computed inside the dq pass
+  // dv computed inside the dk pass: with the roles of (q, dout) and (k, v)
+  // exchanged, dv_n = sum_m Phi g_m is that pass's forward sum
+  bool fused_kv() const { return dk && dv && fuse; }
 };
 
 Want want_for(const gs_problem& p, bool fwd, bool dq, bool dk, bool dv) {
@@ -480,7 +483,7 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   if (wc) pl.v.rt = cv.take<uint16_t>(pl.Np * Wv * 2);
   if (w.fwd && !(w.fused() && p.C == 1)) pl.v.ks = cv.take<uint16_t>(pl.Np * Rv * 2);
   if (wc) pl.g.rt = cv.take<uint16_t>(pl.Mp * Wv * 2);
-  if (w.dv) pl.g.ks = cv.take<uint16_t>(pl.Mp * Rv * 2);
+  if (w.dv && !(w.fused_kv() && p.C == 1)) pl.g.ks = cv.take<uint16_t>(pl.Mp * Rv * 2);
 
   // Partial-sum buffer for split passes (reused by every pass in turn).
   size_t part = 0, part_s = 0;
@@ -496,8 +499,11 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
     const int sp = consider(p.M, p.N, qd, p.D, dq_kernel(p, pl.dm, w.fused()));
     if (w.fused() && sp > 1) part_s = (size_t)sp * p.M * p.C * 4;
   }
-  if (w.dk) consider(p.N, p.M, qd, p.D, dq_kernel(p, pl.dm, false));
-  if (w.dv) consider(p.N, p.M, qf, p.C, kf);
+  if (w.dk) {
+    const int sp = consider(p.N, p.M, qd, p.D, dq_kernel(p, pl.dm, w.fused_kv()));
+    if (w.fused_kv() && sp > 1) part_s = std::max(part_s, (size_t)sp * p.N * p.C * 4);
+  }
+  if (w.dv && !w.fused_kv()) consider(p.N, p.M, qf, p.C, kf);
   pl.part = part ? cv.take<float>(part) : nullptr;
   pl.part_s = part_s ? cv.take<float>(part_s) : nullptr;
   pl.total = cv.off;
@@ -1065,9 +1071,10 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
   } else {
     // every kernel the passes below launch must exist for this shape
     const Dims dm = dims_of(D, C);
-    if (((w.fwd && !w.fused()) || w.dv) && !fwd_for(*p, dm).launch) return GS_ERR_INTERNAL;
+    if (((w.fwd && !w.fused()) || (w.dv && !w.fused_kv())) && !fwd_for(*p, dm).launch)
+      return GS_ERR_INTERNAL;
     if (w.dq && !dq_for(*p, dm, w.fused()).launch) return GS_ERR_INTERNAL;
-    if (w.dk && !dq_for(*p, dm, false).launch) return GS_ERR_INTERNAL;
+    if (w.dk && !dq_for(*p, dm, w.fused_kv()).launch) return GS_ERR_INTERNAL;
   }
   Plan pl;
   make_plan(*p, w, alias, nullptr, pl, 1);
@@ -1126,15 +1133,15 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
     const uint32_t* kslot = alias ? pl.slots + 2 : pl.slots + 3;
     // full-sample row-bound flags for the forward-kernel passes (fwd, dv)
     if (w.fwd && !w.fused()) row_check(c, pl.q, M, pl.Mp, pl.k);
-    if (w.dv && !(alias && w.fwd && !w.fused())) row_check(c, pl.k, N, pl.Np, pl.q);
+    if (w.dv && !w.fused_kv() && !(alias && w.fwd && !w.fused())) row_check(c, pl.k, N, pl.Np, pl.q);
     if (w.fwd && !w.fused()) pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out_, os);
     if (w.dq)
       pass_dq(c, pl.q, M, pl.k, N, pl.scal_kv, kslot, pl.v.rt, pl.slots + 0, pl.g.rt, pl.slots + 1, g_,
               dout_dtype, gst, dq_, dqs, pl.v.ks, w.fused() ? out_ : nullptr, os);
     if (w.dk)
       pass_dq(c, pl.k, N, pl.q, M, pl.scal_qg, pl.slots + 2, pl.g.rt, pl.slots + 1, pl.v.rt,
-              pl.slots + 0, v_, p->v_dtype, vst, dk_, dks);
-    if (w.dv) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv_, dvs);
+              pl.slots + 0, v_, p->v_dtype, vst, dk_, dks, pl.g.ks, w.fused_kv() ? dv_ : nullptr, dvs);
+    if (w.dv && !w.fused_kv()) pass_fwd(c, pl.k, N, pl.q, M, pl.scal_qg, pl.g.ks, pl.slots + 1, dv_, dvs);
   }
   return launch_status();
 }
@@ -1314,4 +1321,29 @@ gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, cons
   }
 }
 
+size_t gauss_sum_fwd_bwd_batched_workspace_size(const gs_problem* p, int64_t count, int want_dq,
+                                                int want_dk, int want_dv) {
+  try {
+    return workspace_for(p, true, want_dq, want_dk, want_dv, count);
+  } catch (...) {
+    return 0;
+  }
+}
+gs_status gauss_sum_fwd_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
+                                    const void* k, const void* v, float tau, const void* dout,
+                                    gs_dtype dout_dtype, float* out, float* dq, float* dk, float* dv,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  try {
+    if (!batch || (!out && batch->count > 0)) {
+      gs_status st = check_problem(p);
+      if (st != GS_SUCCESS) return st;
+      if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+      return GS_ERR_NULL_POINTER;
+    }
+    return run(p, batch, q, k, v, tau, dout, dout_dtype, out, dq, dk, dv, workspace,
+               workspace_bytes, stream);
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
 }  // extern "C"

@@ -36,7 +36,8 @@ EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_bwd", "gauss_sum_fw
             "gauss_sum_status_string", "gauss_sum_abi_version", "gauss_sum_profile_start",
             "gauss_sum_profile_stop", "gauss_sum_mmd_flow", "gauss_sum_mmd_flow_workspace_size",
             "gauss_sum_fwd_batched", "gauss_sum_bwd_batched", "gauss_sum_fwd_batched_workspace_size",
-            "gauss_sum_bwd_batched_workspace_size")
+            "gauss_sum_bwd_batched_workspace_size", "gauss_sum_fwd_bwd_batched",
+            "gauss_sum_fwd_bwd_batched_workspace_size")
 PROFILE_FWD, PROFILE_GRAD = 1, 2
 
 
@@ -97,6 +98,12 @@ def load(path=LIB_PATH):
     lib.gauss_sum_bwd_batched_workspace_size.argtypes = [P, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
                                                          ctypes.c_int]
     lib.gauss_sum_bwd_batched_workspace_size.restype = sz
+    lib.gauss_sum_fwd_bwd_batched.argtypes = [P, BP, vp, vp, vp, ctypes.c_float, vp, ctypes.c_int,
+                                              f32p, f32p, f32p, f32p, vp, sz, vp]
+    lib.gauss_sum_fwd_bwd_batched.restype = ctypes.c_int
+    lib.gauss_sum_fwd_bwd_batched_workspace_size.argtypes = [P, ctypes.c_int64, ctypes.c_int,
+                                                             ctypes.c_int, ctypes.c_int]
+    lib.gauss_sum_fwd_bwd_batched_workspace_size.restype = sz
     lib.gauss_sum_mmd_flow.argtypes = [P, vp, vp, ctypes.c_float, f32p, f32p, vp, vp, sz, vp]
     lib.gauss_sum_mmd_flow.restype = ctypes.c_int
     lib.gauss_sum_mmd_flow_workspace_size.argtypes = [P]
@@ -368,6 +375,50 @@ def gauss_sum_bwd_batched(q, k, v, tau, dout, want=(True, True, True), workspace
     if st != 0:
         raise GaussSumError(st, "gauss_sum_bwd_batched")
     return dq, dk, dv
+
+
+def gauss_sum_fwd_bwd_batched_workspace_size(M, N, D, C, count, qk_dtype=GS_F16, v_dtype=GS_F32,
+                                             want_dq=True, want_dk=True, want_dv=True):
+    p = make_problem(M, N, D, C, qk_dtype, v_dtype)
+    return int(load().gauss_sum_fwd_bwd_batched_workspace_size(ctypes.byref(p), int(count),
+                                                               int(bool(want_dq)), int(bool(want_dk)),
+                                                               int(bool(want_dv))))
+
+
+def gauss_sum_fwd_bwd_batched(q, k, v, tau, dout, want=(True, True, True), out=None, workspace=None,
+                              stream=None, group=None):
+    """(s, dq, dk, dv) of B independent problems in one call (shapes as in
+    gauss_sum_bwd_batched; s is B x M x C); the forward sums ride along in the
+    dq passes where gauss_sum_fwd_bwd fuses them."""
+    import torch
+    B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
+    if not dout.is_cuda or dout.shape != (B, M, C) or not dout.is_contiguous():
+        raise ValueError("dout must be a contiguous %d x %d x %d GPU tensor" % (B, M, C))
+    if (want[1] and ks == 0) or (want[2] and vs == 0):
+        raise ValueError("dk / dv of a shared key set: sum the per-problem gradients instead")
+    p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
+    lib = load()
+    dev = q.device
+    if out is None:
+        out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
+    dq = torch.empty((B, M, D), dtype=torch.float32, device=dev) if want[0] else None
+    dk = torch.empty((B, N, D), dtype=torch.float32, device=dev) if want[1] else None
+    dv = torch.empty((B, N, C), dtype=torch.float32, device=dev) if want[2] else None
+    b = Batch(B, qs, ks, vs, M * C, M * C, M * D, N * D, N * C)
+    need = int(lib.gauss_sum_fwd_bwd_batched_workspace_size(ctypes.byref(p), int(group or max(B, 1)),
+                                                            int(bool(want[0])), int(bool(want[1])),
+                                                            int(bool(want[2]))))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, dev)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_fwd_bwd_batched(ctypes.byref(p), ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v),
+                                       float(tau), _ptr(dout), _dtype_code(dout.dtype), _ptr(out),
+                                       _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), wbytes,
+                                       _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_fwd_bwd_batched")
+    return out, dq, dk, dv
 
 
 def gauss_sum_mmd_flow_workspace_size(N, D, qk_dtype=GS_F16, v_dtype=GS_F32):

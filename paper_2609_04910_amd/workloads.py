@@ -202,6 +202,9 @@ BATCHED = {
     # the N sweep with several channels (B = 4, D = C = 32), at N = 16384
     "batch_c32": dict(B=4, M=16384, N=16384, D=32, C=32),
     "batch_c32_f32": dict(B=4, M=16384, N=16384, D=32, C=32, qk="f32"),
+    # the N sweep of the forward-plus-backward benchmark (B = 4, D = 32,
+    # C = 1, fp16) at N = 65536: s and the gradients with respect to q, k, v
+    "batch_grad_d32": dict(B=4, M=65536, N=65536, D=32, C=1, grad=True),
 }
 
 
@@ -226,6 +229,15 @@ def make_batch(name: str, seed: int = 0, B: Optional[int] = None, M: Optional[in
         k[b] = (rng.standard_normal((N_, D_), dtype=np.float32) * s).astype(pt)
     v = rng.standard_normal((B_, N_, C_), dtype=np.float32)
     return q, k, v, np.float32(1.0)
+
+
+def batch_dout(name: str, seed: int = 0, M: Optional[int] = None) -> np.ndarray:
+    """Upstream gradient dout ~ N(0, 1) fp32 (B x M x C) of a batched
+    workload's backward pass, from its own generator (seed + 1), so the
+    points and values of make_batch stay the same draws."""
+    cfg = BATCHED[name]
+    rng = np.random.default_rng(seed + 1)
+    return rng.standard_normal((cfg["B"], M or cfg["M"], cfg["C"]), dtype=np.float32)
 
 
 def sample_rows(n_total: int, count: int, seed: int = 1, tile: int = 256) -> np.ndarray:

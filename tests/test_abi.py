@@ -169,6 +169,33 @@ def test_bwd_batched_validation():
                                      FAKE + 0x40000 + 64, None, *ws) == 9
 
 
+def test_fwd_bwd_batched_validation():
+    lib = gs.load()
+    prob = gs.make_problem(8, 8, 4, 2, gs.GS_F16, gs.GS_F32)
+    b = gs.Batch(2, 32, 32, 16, 16, 16, 32, 32, 16)
+    args = [FAKE, FAKE + 0x10000, FAKE + 0x20000, ctypes.c_float(1.0), FAKE + 0x70000, gs.GS_F32]
+    ws = [FAKE + 0x100000, 1 << 40, None]
+    fn = lib.gauss_sum_fwd_bwd_batched
+    assert fn(ctypes.byref(prob), None, *args, FAKE + 0x30000, None, None, None, *ws) == 1
+    assert fn(ctypes.byref(prob), ctypes.byref(b), *args, None, FAKE + 0x40000, None, None, *ws) == 1
+    empty = gs.Batch(0, 32, 32, 16, 16, 16, 32, 32, 16)
+    assert fn(ctypes.byref(prob), ctypes.byref(empty), *args, None, None, None, None, *ws) == 0
+    neg = gs.Batch(-1, 32, 32, 16, 16, 16, 32, 32, 16)
+    assert fn(ctypes.byref(prob), ctypes.byref(neg), *args, None, None, None, None, *ws) == 2
+    bad = gs.Batch(2, 32, 32, 16, 16, 15, 32, 32, 16)  # s of problem 1 would overlap problem 0
+    assert fn(ctypes.byref(prob), ctypes.byref(bad), *args, FAKE + 0x30000, FAKE + 0x40000, None,
+              None, *ws) == 2
+    assert fn(ctypes.byref(prob), ctypes.byref(b), *args, FAKE + 0x30000, FAKE + 0x30000 + 64, None,
+              None, *ws) == 9
+    assert fn(ctypes.byref(prob), ctypes.byref(b), *args, FAKE + 0x30000, FAKE + 0x40000, None,
+              None, FAKE + 0x100000, 16, None) == 6
+    one = gs.gauss_sum_fwd_bwd_workspace_size(1000, 3000, 64, 1, want_dk=False, want_dv=False)
+    assert gs.gauss_sum_fwd_bwd_batched_workspace_size(1000, 3000, 64, 1, 1, want_dk=False,
+                                                       want_dv=False) == one
+    assert gs.gauss_sum_fwd_bwd_batched_workspace_size(1000, 3000, 64, 1, 4, want_dk=False,
+                                                       want_dv=False) == 4 * one
+
+
 def test_empty_query_set_is_a_noop():
     # M = 0: nothing to compute; no pointer is touched and no kernel runs.
     assert _fwd(M=0, q=None, out=None) == 0

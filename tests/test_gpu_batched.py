@@ -106,6 +106,32 @@ def test_one_slice_workspace_equals_single_calls(B, M, N, D, C):
             assert torch.equal(x[b], y)
 
 
+@pytest.mark.parametrize("B,M,N,D,C", [SHAPES[0], SHAPES[1], (4, 257, 1500, 32, 1)])
+def test_fwd_bwd_batched(B, M, N, D, C):
+    """gauss_sum_fwd_bwd_batched: every problem against the oracle (all four
+    outputs, one launch group), bitwise equal to the single-problem
+    gauss_sum_fwd_bwd calls with a one-slice workspace, and to a repeat."""
+    import torch
+    from paper_2609_04910_amd import gauss_sum as gs
+    q, k, v, g = clouds(B * 100 + D + 7, B, M, N, D, C)
+    tq, tk, tv, tg = (parity.to_torch(a) for a in (q, k, v, g))
+    tau = 1.0
+    res = gs.gauss_sum_fwd_bwd_batched(tq, tk, tv, tau, tg)
+    torch.cuda.synchronize()
+    for b in range(B):
+        check_problem("fwd_bwd_batched", b, q, k, v, g, tau, *res)
+    again = gs.gauss_sum_fwd_bwd_batched(tq, tk, tv, tau, tg)
+    one = gs.gauss_sum_fwd_bwd_batched(tq, tk, tv, tau, tg, want=(True, False, False), group=1)
+    torch.cuda.synchronize()
+    for x, y in zip(res, again):
+        assert torch.equal(x, y)
+    assert one[2] is None and one[3] is None
+    for b in range(B):
+        s1, dq1, _, _ = gs.gauss_sum_fwd_bwd(tq[b], tk[b], tv[b], tau, tg[b], want=(True, False, False))
+        torch.cuda.synchronize()
+        assert torch.equal(one[0][b], s1) and torch.equal(one[1][b], dq1)
+
+
 def test_every_group_size():
     """B = 5 with room for 1 .. 5 problems per launch: each grouping matches the oracle."""
     import torch
