@@ -659,8 +659,12 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
     for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + j) * 4 + g];
     if constexpr (CW == 0) {
       // single channel: the score MFMAs of all query tiles, then their
-      // exponentials, then the contractions over keys and the row sums, kept
-      // apart by scheduling barriers (2 % faster than tile by tile)
+      // exponentials, then the contractions over keys, kept apart by
+      // scheduling barriers (2 % faster than tile by tile).  The row-sum dot2
+      // instructions go with the contractions for D > 32 (there they cost
+      // nothing) and with the exponentials for D <= 32 (interleaved with the
+      // few contraction MFMAs of a 32-wide step they cost 14 % of the pass,
+      // in the exponential block 8 %)
       floatx4 acc[QT][2];
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt)
@@ -676,13 +680,14 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
           for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[qt][kt][r], tau2, bq[qt]));
         b[qt] = pack_tile_pair(p);
+        if constexpr (DP == 1) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) dQ[qt][dt] = mfma_f16(ktr[dt], b[qt], dQ[qt][dt]);
-        rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
+        if constexpr (DP > 1) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
       }
       return;
     }
