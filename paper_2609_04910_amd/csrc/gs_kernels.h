@@ -326,6 +326,26 @@ __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
   return b;
 }
 
+// Rows of `width` floats starting at `base` can take 16-byte stores (every
+// row start 16-byte aligned).
+__device__ __forceinline__ bool vec4_rows(const float* base, int width) {
+  return (width % 4 == 0) && ((reinterpret_cast<uintptr_t>(base) & 15) == 0);
+}
+
+// Elements c0 .. c0+3 of one output row (c0 a multiple of 4) with one 16-byte
+// store when v4, else element by element up to `width`.
+__device__ __forceinline__ void store_row4(float* row, int c0, int width, bool v4, float a, float b,
+                                           float c, float d) {
+  if (v4) {
+    if (c0 < width) *reinterpret_cast<float4*>(row + c0) = float4{a, b, c, d};
+  } else {
+    if (c0 < width) row[c0] = a;
+    if (c0 + 1 < width) row[c0 + 1] = b;
+    if (c0 + 2 < width) row[c0 + 2] = c;
+    if (c0 + 3 < width) row[c0 + 3] = d;
+  }
+}
+
 // ---------------------------------------------------------------- forward
 
 // ONE (single channel, C = 1): the magnitude of v_n enters the exponent via the
@@ -493,6 +513,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     key_stream<NS, NCH + 1>(s_begin, s_end, issue, [&](int st) { compute(st, std::false_type{}); });
 
   const int ev = scale_exponent(*vslot) - (ONE ? 1 : 0);
+  const bool v4 = vec4_rows(out, C);
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int64_t m = q0 + 16 * qt + j;
@@ -500,11 +521,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     const float f = exp2f(off[qt]);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int c = 16 * ct + 4 * g + r;
-        if (c < C) out[m * C + c] = ldexpf(O[qt][ct][r] * f, -ev);
-      }
+      store_row4(out + m * C, 16 * ct + 4 * g, C, v4, ldexpf(O[qt][ct][0] * f, -ev),
+                 ldexpf(O[qt][ct][1] * f, -ev), ldexpf(O[qt][ct][2] * f, -ev), ldexpf(O[qt][ct][3] * f, -ev));
   }
 }
 
@@ -744,13 +762,12 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
         if (g == 0) out_s[m] = ldexpf(rs[qt] * f, 1 - scale_exponent(*vslot));
       } else {
         const int ev = scale_exponent(*vslot);
+        const bool v4 = vec4_rows(out_s, C);
 #pragma unroll
         for (int ct = 0; ct < FCH; ++ct)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int c = 16 * ct + 4 * g + r;
-            if (c < C) out_s[m * C + c] = ldexpf(O[qt][ct][r] * f, -ev);
-          }
+          store_row4(out_s + m * C, 16 * ct + 4 * g, C, v4, ldexpf(O[qt][ct][0] * f, -ev),
+                     ldexpf(O[qt][ct][1] * f, -ev), ldexpf(O[qt][ct][2] * f, -ev),
+                     ldexpf(O[qt][ct][3] * f, -ev));
       }
     }
   }
@@ -768,17 +785,20 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
       f *= load_any(g1, m, g1_dtype);
     }
     const float rm = rs[qt];
+    const bool v4d = vec4_rows(out, D);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+    for (int dt = 0; dt < DT; ++dt) {
+      const int d0 = 16 * dt + 4 * g;
+      if (d0 >= D) continue;
+      // q_m,d0 .. d0+3 from the RT copy: four consecutive halves (8 bytes)
+      const uint2 qq = *reinterpret_cast<const uint2*>(q16 + rt_index(m, d0, 32 * DP));
+      const float qv[4] = {T::to_float((uint16_t)qq.x), T::to_float((uint16_t)(qq.x >> 16)),
+                           T::to_float((uint16_t)qq.y), T::to_float((uint16_t)(qq.y >> 16))};
+      float o[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int d = 16 * dt + 4 * g + r;
-        if (d < D) {
-          const float qv = T::to_float(q16[rt_index(m, d, 32 * DP)]);
-          const float val = ldexpf(dQ[qt][dt][r], -ek) - qv * rm;
-          out[m * D + d] = ldexpf(val * f, e);
-        }
-      }
+      for (int r = 0; r < 4; ++r) o[r] = ldexpf((ldexpf(dQ[qt][dt][r], -ek) - qv[r] * rm) * f, e);
+      store_row4(out + m * D, d0, D, v4d, o[0], o[1], o[2], o[3]);
+    }
   }
 }
 
