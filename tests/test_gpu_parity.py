@@ -80,6 +80,31 @@ def test_same_points_alias_matches_separate_arrays():
     parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
 
 
+@pytest.mark.parametrize("D,C", [(24, 1), (40, 9), (128, 16), (130, 16), (64, 17)])
+def test_dv_alone_and_fused_into_dk(D, C):
+    """dv requested alone (its own forward-type pass) and together with dk
+    (where the forward fusion applies, C = 1 or C <= 16 and D <= 128, the dk
+    pass forms it as its forward sum): both match the oracle, and dk does not
+    depend on whether dv rides along."""
+    import torch
+    import parity
+    from paper_2609_04910_amd import gauss_sum as gs
+    w = parity.random_workload(31 + D + C, 257, 700, D, C)
+    q, k, v, g = parity.gpu_inputs(w, alias=False)
+    _, _, dv_alone = gs.gauss_sum_bwd(q, k, v, float(w.tau), g, want=(False, False, True))
+    _, dk_only, _ = gs.gauss_sum_bwd(q, k, v, float(w.tau), g, want=(False, True, False))
+    _, dk, dv = gs.gauss_sum_bwd(q, k, v, float(w.tau), g, want=(False, True, True))
+    torch.cuda.synchronize()
+    assert torch.equal(dk, dk_only)
+    import oracle
+    th = parity.oracle_threads()
+    ref, scale = oracle.dv(w.q_values, w.k_values, w.v, w.g, float(w.tau), threads=th)
+    for label, got in (("dv alone", dv_alone), ("dv with dk", dv)):
+        _say(label, D, C, parity.compare(label, got.cpu().numpy(), ref, scale, parity.TOL["f16"]))
+    ref, scale = oracle.dk(w.q_values, w.k_values, w.v, w.g, float(w.tau), threads=th)
+    parity.compare("dk", dk.cpu().numpy(), ref, scale, parity.TOL["f16"])
+
+
 def test_deterministic_bitwise():
     import parity
     w = parity.random_workload(6, 2000, 3000, 48, 8)
