@@ -397,6 +397,53 @@ def bench_batched_grad(args):
     print(json.dumps(res), flush=True)
 
 
+def bench_svgd_update(args):
+    """One gauss_sum_svgd call per step on the svgd workload's particles and
+    score-like values (the SVGD direction of Sec. 3: forward sum with values
+    score plus the repulsive query-gradient term); prints one JSON line with
+    the step time and pairs/s (N^2 per step).  A secondary measurement, not
+    the benchmark line."""
+    import numpy as np
+    import torch
+
+    from paper_2609_04910_amd import gauss_sum as gs
+    from paper_2609_04910_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    w = wl.make("svgd", seed=0)
+    x = torch.from_numpy(w.q).to(dev)
+    sc = torch.from_numpy(np.ascontiguousarray(w.v)).to(dev)
+    ws = torch.empty(max(gs.gauss_sum_svgd_workspace_size(w.N, w.D, gs.GS_F16, gs.GS_F16), 1),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty((w.N, w.D), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gs.gauss_sum_svgd(x, sc, float(w.tau), out=out, workspace=ws, stream=stream)
+
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < args.settle_ms:
+        step()
+        torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    print(json.dumps({"mode": "svgd_update", "unit": "pairs/s", "data": "synthetic",
+                      "config": {"workload": "svgd particles: N=%d, D=%d, f16, score-like values -x + "
+                                             "0.1 eps (f16), tau=%g" % (w.N, w.D, float(w.tau)),
+                                 "api": "gauss_sum_svgd"},
+                      "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+                      "pairs_per_s": float(w.N) * w.N / (ms * 1e-3)}), flush=True)
+
+
 def compare_attention_grad(args):
     """The paper's gradient route on this GPU, as an external comparison (not
     part of the library): Alg. 2 (reweight) through PyTorch's public
@@ -694,6 +741,9 @@ def main():
                          "Alg. 2 with autograd) beside the library")
     ap.add_argument("--batch-n", type=int, default=None, metavar="N",
                     help="--compare-attention on batch_grad_d32: M = N = this instead of 65536")
+    ap.add_argument("--svgd-update", action="store_true",
+                    help="time gauss_sum_svgd (one SVGD direction per step) on the svgd workload's "
+                         "particles and score-like values")
     ap.add_argument("--separate", action="store_true",
                     help="time separate gauss_sum_fwd + gauss_sum_bwd calls instead of one "
                          "gauss_sum_fwd_bwd call")
@@ -721,6 +771,9 @@ def main():
     gs.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.svgd_update:
+        bench_svgd_update(args)
+        return
     if args.compare_attention:
         if args.workload not in wl.BATCHED:
             print("--compare-attention takes a batched workload (--workload batch_d32)", file=sys.stderr)

@@ -218,6 +218,25 @@ gs_status gauss_sum_mmd_flow(const gs_problem* p, const void* x, const void* v, 
 /* Bytes of device workspace gauss_sum_mmd_flow needs (0 if p is invalid for it). */
 size_t gauss_sum_mmd_flow_workspace_size(const gs_problem* p);
 
+/* One Stein variational gradient descent update (Sec. 3, the MMD-flow and
+ * SVGD paragraph: the kernel part of the SVGD direction has the same form as
+ * the query gradient): particles x (N x D, qk_dtype) and the scores
+ * score_n = grad log p(x_n) (N x D, v_dtype) give, for m < N,
+ *   phi[m, :] = sum_n Phi(x_m, x_n) score_n + tau sum_n Phi(x_m, x_n) (x_m - x_n)
+ * (fp32, N x D), the SVGD direction without its 1/N factor (the second sum is
+ * the gradient of sum_n Phi(x_n, x_m) with respect to x_n, summed: the
+ * repulsive term).  Computed as the forward sum with values score and the
+ * query-gradient pass with unit weights.  Requires p->M == p->N and
+ * p->C == p->D (GS_ERR_BAD_SHAPE); fp16 or bf16 points.  phi must not overlap
+ * x, score or the workspace.  N == 0 is a no-op.  Workspace:
+ * gauss_sum_svgd_workspace_size. */
+gs_status gauss_sum_svgd(const gs_problem* p, const void* x, const void* score, float tau, float* phi,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes for gauss_sum_svgd; 0 if p does not describe an SVGD
+ * update (M != N, C != D, invalid, or fp32 points) or N == 0. */
+size_t gauss_sum_svgd_workspace_size(const gs_problem* p);
+
 /* Static, never-NULL description of a status code. */
 const char* gauss_sum_status_string(gs_status s);
 

@@ -1210,6 +1210,67 @@ gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, c
   }
 }
 
+// SVGD: workspace = unit weights (N floats) and the query-gradient buffer
+// (N x D floats), then room for the larger of the two passes.
+size_t svgd_extra(int64_t n, int64_t D) {
+  return (size_t)(gs::round_up(std::max<int64_t>(n, 1) * 4, 256) +
+                  gs::round_up(std::max<int64_t>(n, 1) * D * 4, 256));
+}
+gs_problem svgd_flow_problem(const gs_problem* p) {
+  gs_problem q = *p;
+  q.C = 1;
+  q.v_dtype = GS_F32;
+  return q;
+}
+size_t gauss_sum_svgd_workspace_size(const gs_problem* p) {
+  if (!p || gs::check_problem(p) != GS_SUCCESS || p->M != p->N || p->C != p->D ||
+      p->qk_dtype == GS_F32 || p->N == 0)
+    return 0;
+  const gs_problem q = svgd_flow_problem(p);
+  return svgd_extra(p->N, p->D) +
+         std::max(gs::workspace_for(p, true, 0, 0, 0), gs::workspace_for(&q, false, 1, 0, 0));
+}
+gs_status gauss_sum_svgd(const gs_problem* p, const void* x, const void* score, float tau, float* phi,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  using namespace gs;
+  try {
+    gs_status st = check_problem(p);
+    if (st != GS_SUCCESS) return st;
+    if ((st = check_tau(tau)) != GS_SUCCESS) return st;
+    if (p->M != p->N || p->C != p->D) return GS_ERR_BAD_SHAPE;
+    if (p->qk_dtype == GS_F32) return GS_ERR_UNSUPPORTED;
+    if (!phi) return GS_ERR_NULL_POINTER;
+    const int64_t n = p->N, D = p->D;
+    if (n > 0 && (!x || !score)) return GS_ERR_NULL_POINTER;
+    if (!aligned(phi, 4)) return GS_ERR_MISALIGNED;
+    if (n == 0) return GS_SUCCESS;
+    const size_t need = gauss_sum_svgd_workspace_size(p);
+    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_SUCCESS) return st;
+    const Range in[3] = {range_of(x, n * D * 2), range_of(score, n * D * (int64_t)dsize(p->v_dtype)),
+                         range_of(workspace, (int64_t)need)};
+    for (int b = 0; b < 3; ++b)
+      if (overlap(range_of(phi, n * D * 4), in[b])) return GS_ERR_ALIAS;
+    char* base = static_cast<char*>(workspace);
+    float* ones = reinterpret_cast<float*>(base);
+    float* flow = reinterpret_cast<float*>(base + round_up(std::max<int64_t>(n, 1) * 4, 256));
+    const size_t extra = svgd_extra(n, D);
+    // phi = sum_n Phi(x_m, x_n) score_n
+    st = run(p, nullptr, x, x, score, tau, nullptr, GS_F32, phi, nullptr, nullptr, nullptr, base + extra,
+             workspace_bytes - extra, stream);
+    if (st != GS_SUCCESS) return st;
+    // flow = tau sum_n Phi (x_n - x_m): the query gradient with unit weights
+    // and unit upstream gradient
+    const gs_problem q = svgd_flow_problem(p);
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid1(n)), dim3(256), 0, stream, ones, n, 1.0f);
+    st = run(&q, nullptr, x, x, ones, tau, ones, GS_F32, nullptr, flow, nullptr, nullptr, base + extra,
+             workspace_bytes - extra, stream);
+    if (st != GS_SUCCESS) return st;
+    hipLaunchKernelGGL(k_sub_f32, dim3(grid1(n * D)), dim3(256), 0, stream, phi, (const float*)flow, n * D);
+    return launch_status();
+  } catch (...) {
+    return GS_ERR_INTERNAL;
+  }
+}
 size_t gauss_sum_mmd_flow_workspace_size(const gs_problem* p) {
   if (!p || gs::check_problem(p) != GS_SUCCESS || p->M != p->N || p->C != 1 || p->qk_dtype == GS_F32)
     return 0;

@@ -37,7 +37,7 @@ EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_bwd", "gauss_sum_fw
             "gauss_sum_profile_stop", "gauss_sum_mmd_flow", "gauss_sum_mmd_flow_workspace_size",
             "gauss_sum_fwd_batched", "gauss_sum_bwd_batched", "gauss_sum_fwd_batched_workspace_size",
             "gauss_sum_bwd_batched_workspace_size", "gauss_sum_fwd_bwd_batched",
-            "gauss_sum_fwd_bwd_batched_workspace_size")
+            "gauss_sum_fwd_bwd_batched_workspace_size", "gauss_sum_svgd", "gauss_sum_svgd_workspace_size")
 PROFILE_FWD, PROFILE_GRAD = 1, 2
 
 
@@ -105,6 +105,10 @@ def load(path=LIB_PATH):
                                                              ctypes.c_int, ctypes.c_int]
     lib.gauss_sum_fwd_bwd_batched_workspace_size.restype = sz
     lib.gauss_sum_mmd_flow.argtypes = [P, vp, vp, ctypes.c_float, f32p, f32p, vp, vp, sz, vp]
+    lib.gauss_sum_svgd.argtypes = [P, vp, vp, ctypes.c_float, f32p, vp, sz, vp]
+    lib.gauss_sum_svgd.restype = ctypes.c_int
+    lib.gauss_sum_svgd_workspace_size.argtypes = [P]
+    lib.gauss_sum_svgd_workspace_size.restype = sz
     lib.gauss_sum_mmd_flow.restype = ctypes.c_int
     lib.gauss_sum_mmd_flow_workspace_size.argtypes = [P]
     lib.gauss_sum_mmd_flow_workspace_size.restype = sz
@@ -451,6 +455,37 @@ def gauss_sum_mmd_flow(x, v, tau, want=(True, True, True), workspace=None, strea
     if st != 0:
         raise GaussSumError(st, "gauss_sum_mmd_flow")
     return s, grad, mmd2
+
+
+def gauss_sum_svgd_workspace_size(N, D, qk_dtype=GS_F16, v_dtype=GS_F32):
+    p = make_problem(N, N, D, D, qk_dtype, v_dtype)
+    return int(load().gauss_sum_svgd_workspace_size(ctypes.byref(p)))
+
+
+def gauss_sum_svgd(x, score, tau, out=None, workspace=None, stream=None):
+    """One SVGD update direction (without the 1/N factor) for particles x
+    (N x D) and scores score = grad log p(x) (N x D):
+    phi[m] = sum_n Phi(x_m, x_n) score_n + tau sum_n Phi(x_m, x_n) (x_m - x_n)."""
+    import torch
+    _check_inputs(x, x, score)
+    N, D = x.shape
+    if score.shape != (N, D):
+        raise ValueError("score must be N x D")
+    p = make_problem(N, N, D, D, _dtype_code(x.dtype), _dtype_code(score.dtype))
+    lib = load()
+    dev = x.device
+    if out is None:
+        out = torch.empty((N, D), dtype=torch.float32, device=dev)
+    need = int(lib.gauss_sum_svgd_workspace_size(ctypes.byref(p)))
+    if workspace is None:
+        workspace, wbytes = _workspace(need, dev)
+    else:
+        wbytes = workspace.numel() * workspace.element_size()
+    st = lib.gauss_sum_svgd(ctypes.byref(p), _ptr(x), _ptr(score), float(tau), _ptr(out), _ptr(workspace),
+                            wbytes, _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_svgd")
+    return out
 
 
 def _make_autograd():

@@ -196,6 +196,30 @@ def test_fwd_bwd_batched_validation():
                                                        want_dv=False) == 4 * one
 
 
+def test_svgd_validation():
+    lib = gs.load()
+    F16 = gs.GS_F16
+
+    def call(M=64, N=64, D=8, C=8, qk=F16, x=FAKE, sc=FAKE + 0x10000, tau=1.0, phi=FAKE + 0x20000,
+             ws=FAKE + 0x100000, wsb=1 << 40):
+        prob = gs.make_problem(M, N, D, C, qk, gs.GS_F32)
+        return lib.gauss_sum_svgd(ctypes.byref(prob), x, sc, ctypes.c_float(tau), phi, ws, wsb, None)
+
+    assert call(N=63) == 2 and call(C=7) == 2 and call(D=300, C=300) == 2
+    assert call(tau=0.0) == 3
+    assert call(qk=gs.GS_F32) == 4
+    assert call(phi=None) == 1 and call(x=None) == 1 and call(sc=None) == 1
+    assert call(phi=FAKE + 0x20002) == 5
+    assert call(phi=FAKE + 8) == 9               # phi meets x
+    assert call(phi=FAKE + 0x100000 + 64) == 9   # phi inside the workspace
+    assert call(wsb=16) == 6
+    assert call(M=0, N=0, x=None, sc=None, ws=None, wsb=0) == 0
+    w = gs.gauss_sum_svgd_workspace_size(1000, 64)
+    assert w > 0 and w % 256 == 0
+    assert w >= 1000 * 64 * 4 + gs.gauss_sum_fwd_workspace_size(1000, 1000, 64, 64)
+    assert gs.gauss_sum_svgd_workspace_size(1000, 64, gs.GS_F32) == 0
+
+
 def test_empty_query_set_is_a_noop():
     # M = 0: nothing to compute; no pointer is touched and no kernel runs.
     assert _fwd(M=0, q=None, out=None) == 0
