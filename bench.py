@@ -48,6 +48,11 @@ if ROOT not in sys.path:
 
 METRIC = "Gauss-sum pair interactions/sec (M·N/s) fwd+bwd; % of fp16 MFMA peak"
 PEAK_MFMA_F16 = 2.5e15  # MI355X dense fp16 / bf16 matrix peak, flop/s
+# v_exp_f32 at a quarter of the fp32 lane rate: the published 157.3 TFLOP/s fp32
+# vector peak is 256 CUs x 4 SIMDs x 32 lanes x 2 flop x 2.4 GHz, so a quarter
+# rate is 8 exponentials per SIMD and clock
+EXP_NOMINAL = 256 * 4 * 32 / 4 * 2.4e9
+PEAKS_FILE = os.path.join(ROOT, "profiles", "peaks_mi355x.json")
 
 PASSES = {
     "dense_d16": ("fwd",),
@@ -138,6 +143,49 @@ def recorded_traffic(workload, dominant):
     if rec.get("kernel") != dominant or rec.get("kernel_sources_sha256") != kernel_sources_hash():
         return None
     return rec.get("bytes_per_launch")
+
+
+def measured_peaks():
+    """Rates measured on an MI355X by `bench.py --peaks` (libgs_peaks.so), or None."""
+    try:
+        with open(PEAKS_FILE) as fh:
+            return json.load(fh)
+    except (OSError, ValueError):
+        return None
+
+
+def measured_mfma(achieved_tflops):
+    """The dominant kernel's throughput against the measured 16x16x32 f16 MFMA rate."""
+    pk = measured_peaks()
+    if not pk:
+        return {}
+    m = pk["mfma_f16_16x16x32_flop_per_s"] / 1e12
+    return {"peak_measured": m, "frac_of_measured": achieved_tflops / m}
+
+
+def exp_rate(pairs_per_launch, avg_ms):
+    """Exponentials per second of the dominant kernel (one exp2 per pair and
+    launch) against the nominal and the measured v_exp_f32 rates."""
+    got = pairs_per_launch / (avg_ms * 1e-3)
+    out = {"achieved": got, "unit": "exp/s", "peak_nominal": EXP_NOMINAL, "frac_nominal": got / EXP_NOMINAL}
+    pk = measured_peaks()
+    if pk:
+        out["peak_measured"] = pk["exp2_per_s"]
+        out["frac_measured"] = got / pk["exp2_per_s"]
+    return out
+
+
+def bench_peaks(args):
+    """Measure the device's own rates with libgs_peaks.so and print them as one
+    JSON line (the record profiles/peaks_mi355x.json holds)."""
+    import torch
+
+    from paper_2609_04910_amd import peaks
+
+    rec = peaks.measure()
+    rec.update({"device": torch.cuda.get_device_name(0), "mfma_nominal_flop_per_s": PEAK_MFMA_F16,
+                "exp2_nominal_per_s": EXP_NOMINAL, "hbm_nominal_bytes_per_s": 8e12})
+    print(json.dumps(rec), flush=True)
 
 
 def describe(w, passes):
@@ -284,6 +332,9 @@ def bench_batched(args):
                      "flops_per_launch": per_launch,
                      "launch_share_of_step": avg * per_step / ms_per_step},
     }
+    if not f32:
+        res["roofline"].update(measured_mfma(achieved))
+    res["roofline"]["exp"] = exp_rate(float(B) / per_step * M * N, avg)
     if not args.no_cpu:
         threads = min(oracle.default_threads(), 16)
         oracle.fwd(q[0], k[0], v[0], float(tau), rows=np.arange(1), threads=threads)
@@ -376,6 +427,9 @@ def bench_batched_grad(args):
                      "launches_per_step": per_step, "flops_per_step": grad_flops,
                      "launch_share_of_step": grad_ms / ms_per_step},
     }
+    res["roofline"].update(measured_mfma(res["roofline"]["achieved"]))
+    # two passes over every pair per step (dq, dk), one exponential each
+    res["roofline"]["exp"] = exp_rate(2.0 * pairs / per_step, grad_ms / per_step)
     if not args.no_cpu:
         threads = min(oracle.default_threads(), 16)
         rows = wl.sample_rows(M, 64, seed=5)
@@ -741,6 +795,8 @@ def main():
                          "Alg. 2 with autograd) beside the library")
     ap.add_argument("--batch-n", type=int, default=None, metavar="N",
                     help="--compare-attention on batch_grad_d32: M = N = this instead of 65536")
+    ap.add_argument("--peaks", action="store_true",
+                    help="measure the device's MFMA, exp2, FMA and streaming-read rates and exit")
     ap.add_argument("--svgd-update", action="store_true",
                     help="time gauss_sum_svgd (one SVGD direction per step) on the svgd workload's "
                          "particles and score-like values")
@@ -771,6 +827,9 @@ def main():
     gs.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.peaks:
+        bench_peaks(args)
+        return
     if args.svgd_update:
         bench_svgd_update(args)
         return
@@ -922,6 +981,8 @@ def main():
             "flops_per_launch": dom_flops,
         },
     }
+    res["roofline"].update(measured_mfma(achieved))
+    res["roofline"]["exp"] = exp_rate(pairs, avg_kernel_ms)
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(w, passes, args.cpu_budget)
     print(json.dumps(res), flush=True)

@@ -1,4 +1,6 @@
-"""Build the gfx950 HIP library libgauss_sum.so in-tree (hipcc, no JIT cache).
+"""Build the gfx950 HIP libraries in-tree (hipcc, no JIT cache): libgauss_sum.so
+(the Gauss-sum kernels and their C ABI) and libgs_peaks.so (the rate
+calibration kernels the benchmark measures the device's own rates with).
 
 Flags: -O3 for gfx950 only; packed fp32 instructions are disabled in the
 device code (-Xclang -target-feature -Xclang -packed-fp32-ops).
@@ -10,6 +12,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "gauss_sum.hip")
 LIB = os.path.join(HERE, "libgauss_sum.so")
+PEAKS_SRC = os.path.join(HERE, "peaks", "gs_peaks.hip")
+PEAKS_LIB = os.path.join(HERE, "libgs_peaks.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -24,9 +28,15 @@ FLAGS = [
 
 
 def build(verbose: bool = False) -> str:
-    """Compile csrc/gauss_sum.hip into libgauss_sum.so; returns its path."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-o", tmp, SRC]
+    """Compile csrc/gauss_sum.hip into libgauss_sum.so and peaks/gs_peaks.hip
+    into libgs_peaks.so; returns the path of libgauss_sum.so."""
+    compile_one(PEAKS_SRC, PEAKS_LIB, verbose)
+    return compile_one(SRC, LIB, verbose)
+
+
+def compile_one(src: str, lib: str, verbose: bool) -> str:
+    tmp = lib + ".tmp%d" % os.getpid()
+    cmd = [HIPCC] + FLAGS + ["-o", tmp, src]
     res = subprocess.run(cmd, capture_output=True, text=True)
     noise = "not a recognized feature for this target"
     msgs = "\n".join(ln for ln in (res.stdout + res.stderr).splitlines() if noise not in ln)
@@ -34,8 +44,8 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed (%d):\n%s" % (res.returncode, msgs))
     if verbose and msgs.strip():
         print(msgs)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 def sources():
