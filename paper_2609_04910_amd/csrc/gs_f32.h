@@ -191,6 +191,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32(
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t dlane = dma_lane_offset(lane);
   const int wave = threadIdx.x / kWave;
   const int j = lane & 15, g = lane >> 4;
   const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * (16 * QT);
@@ -211,9 +212,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32(
     const uint32_t base = lds0 + stage * STAGE;
     const uint32_t ls = (uint32_t)(s - s_begin);
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) dma_x4(rkh, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+    for (int c = 0; c < KCH; ++c) dma_x4(rkh, (ls * KCH + c) * 1024, base + c * 1024, dlane);
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) dma_x4(rkl, (ls * KCH + c) * 1024, base + (KCH + c) * 1024, 16 * lane);
+    for (int c = 0; c < KCH; ++c) dma_x4(rkl, (ls * KCH + c) * 1024, base + (KCH + c) * 1024, dlane);
     dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
   };
 
@@ -254,8 +255,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32(
       const floatx4 cin = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
       const floatx4 sg = *reinterpret_cast<const floatx4*>(sc + 32 + 16 * kt + 4 * g);
       uint4 khr[DP], klr[DP];
-      load_k_tile<DP>(khb, kt, j, g, khr);
-      load_k_tile<DP>(klb, kt, j, g, klr);
+      load_k_tile_lds<DP>(khb, kt, j, g, khr);
+      load_k_tile_lds<DP>(klb, kt, j, g, klr);
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) {
         floatx4 acc = cin;
@@ -342,6 +343,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32c(
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t dlane = dma_lane_offset(lane);
   const int wave = threadIdx.x / kWave;
   const int j = lane & 15, g = lane >> 4;
   const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * (16 * QT);
@@ -367,9 +369,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32c(
     const uint32_t base = lds0 + stage * STAGE;
     const uint32_t ls = (uint32_t)(s - s_begin);
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) dma_x4(rkh, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+    for (int c = 0; c < KCH; ++c) dma_x4(rkh, (ls * KCH + c) * 1024, base + c * 1024, dlane);
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) dma_x4(rkl, (ls * KCH + c) * 1024, base + (KCH + c) * 1024, 16 * lane);
+    for (int c = 0; c < KCH; ++c) dma_x4(rkl, (ls * KCH + c) * 1024, base + (KCH + c) * 1024, dlane);
     dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
   };
   auto issue_all = [&](int s, int stage) {
@@ -379,10 +381,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32c(
     const uint32_t ls = (uint32_t)(s - s_begin);
 #pragma unroll
     for (int c = 0; c < CT; ++c)
-      dma_x4(rvh, ls * (uint32_t)vstep + c * 1024, base + (2 * KCH + c) * 1024, 16 * lane);
+      dma_x4(rvh, ls * (uint32_t)vstep + c * 1024, base + (2 * KCH + c) * 1024, dlane);
 #pragma unroll
     for (int c = 0; c < CT; ++c)
-      dma_x4(rvl, ls * (uint32_t)vstep + c * 1024, base + (2 * KCH + CT + c) * 1024, 16 * lane);
+      dma_x4(rvl, ls * (uint32_t)vstep + c * 1024, base + (2 * KCH + CT + c) * 1024, dlane);
   };
 
   const int es = scale_exponent(slots[2]) + scale_exponent(slots[kslot]) + 2 * kSplitHeadroom;
@@ -418,8 +420,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32c(
     for (int kt = 0; kt < 2; ++kt) {
       const floatx4 cin = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
       uint4 khr[DP], klr[DP];
-      load_k_tile<DP>(khb, kt, j, g, khr);
-      load_k_tile<DP>(klb, kt, j, g, klr);
+      load_k_tile_lds<DP>(khb, kt, j, g, khr);
+      load_k_tile_lds<DP>(klb, kt, j, g, klr);
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score(khr, klr, qt, cin)));
     }
@@ -470,16 +472,16 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32c(
     uint4 vhr[CT], vlr[CT];
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
-      vhr[ct] = vhb[(16 * ct + j) * 4 + g];
-      vlr[ct] = vlb[(16 * ct + j) * 4 + g];
+      vhr[ct] = vhb[(16 * ct + j) * 4 + lds_col(j, g)];
+      vlr[ct] = vlb[(16 * ct + j) * 4 + lds_col(j, g)];
     }
     float p[QT][2][4];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       const floatx4 cin = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
       uint4 khr[DP], klr[DP];
-      load_k_tile<DP>(khb, kt, j, g, khr);
-      load_k_tile<DP>(klb, kt, j, g, klr);
+      load_k_tile_lds<DP>(khb, kt, j, g, khr);
+      load_k_tile_lds<DP>(klb, kt, j, g, klr);
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) {
         const floatx4 acc = score(khr, klr, qt, cin);

@@ -171,6 +171,24 @@ __device__ __forceinline__ void load_k_tile(const uint4* base, int64_t tile, int
   for (int dc = 0; dc < DP; ++dc) kr[dc] = base[((tile * DP + dc) * 16 + j) * 4 + g];
 }
 
+// Key-side tiles in LDS are 1-KiB chunks of 16 rows x 64 bytes, and an MFMA
+// operand read (ds_read_b128) has lane (j, g) take the 16-byte column g of
+// row j.  Stored plainly, rows 4 apart share LDS banks and every such read
+// takes two passes; the direct copies therefore store column c of row r at
+// column c ^ ((r >> 1) & 3) (lane l of a copy fetches the global column that
+// belongs in LDS slot l), and readers index through lds_col.  Global copies
+// keep the plain layout.
+__device__ __forceinline__ int lds_col(int j, int g) { return g ^ ((j >> 1) & 3); }
+__device__ __forceinline__ uint32_t dma_lane_offset(int lane) {
+  return 16u * (uint32_t)((lane & ~3) | ((lane ^ (lane >> 3)) & 3));
+}
+template <int DP>
+__device__ __forceinline__ void load_k_tile_lds(const uint4* base, int tile, int j, int g, uint4 (&kr)[DP]) {
+  const int c = lds_col(j, g);
+#pragma unroll
+  for (int dc = 0; dc < DP; ++dc) kr[dc] = base[((tile * DP + dc) * 16 + j) * 4 + c];
+}
+
 // Per-wave prologue of the gradient kernel: the coarse row-bound check.
 // sample_rt / sample_nh: the sampled keys (RT layout, half norms, coarse
 // sample first).  Returns whether some query of the wave has its sampled row
@@ -379,6 +397,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t dlane = dma_lane_offset(lane);
   const int wave = threadIdx.x / kWave;
   const int j = lane & 15, g = lane >> 4;
   const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * (16 * QT);
@@ -400,9 +419,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     const uint32_t base = lds0 + stage * STAGE;
     const uint32_t ls = (uint32_t)(s - s_begin);
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+    for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, dlane);
 #pragma unroll
-    for (int c = 0; c < CT; ++c) dma_x4(rv, (ls * CT + c) * 1024, base + (KCH + c) * 1024, 16 * lane);
+    for (int c = 0; c < CT; ++c) dma_x4(rv, (ls * CT + c) * 1024, base + (KCH + c) * 1024, dlane);
     dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
   };
 
@@ -440,7 +459,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
       const uint32_t base = lds0 + stage * STAGE;
       const uint32_t ls = (uint32_t)(s - s_begin);
 #pragma unroll
-      for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+      for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, dlane);
       dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
     };
     key_stream<NS, KCH + 1>(s_begin, s_end, issue_k, [&](int stage) {
@@ -452,7 +471,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
       for (int kt = 0; kt < 2; ++kt) {
         const floatx4 cin = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
         uint4 kr[DP];
-        load_k_tile<DP>(kb, kt, j, g, kr);
+        load_k_tile_lds<DP>(kb, kt, j, g, kr);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
       }
@@ -486,12 +505,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
-      load_k_tile<DP>(kb, kt, j, g, kr[kt]);
+      load_k_tile_lds<DP>(kb, kt, j, g, kr[kt]);
     }
     uint4 vr[CT];
     const uint4* vb = reinterpret_cast<const uint4*>(base + KCH * 1024);
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) vr[ct] = vb[(16 * ct + j) * 4 + g];
+    for (int ct = 0; ct < CT; ++ct) vr[ct] = vb[(16 * ct + j) * 4 + lds_col(j, g)];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       float p[2][4];
@@ -589,6 +608,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t dlane = dma_lane_offset(lane);
   const int wave = threadIdx.x / kWave;
   const int j = lane & 15, g = lane >> 4;
   const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * (16 * QT);
@@ -615,15 +635,15 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
     const uint32_t base = lds0 + stage * STAGE;
     const uint32_t ls = (uint32_t)(s - s_begin);
 #pragma unroll
-    for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, 16 * lane);
+    for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, dlane);
 #pragma unroll
-    for (int c = 0; c < VCH; ++c) dma_x4(rv, (ls * VCH + c) * 1024, base + (KCH + c) * 1024, 16 * lane);
+    for (int c = 0; c < VCH; ++c) dma_x4(rv, (ls * VCH + c) * 1024, base + (KCH + c) * 1024, dlane);
 #pragma unroll
     for (int c = 0; c < TCH; ++c)
-      dma_x4(rt, (ls * TCH + c) * 1024, base + (KCH + VCH + c) * 1024, 16 * lane);
+      dma_x4(rt, (ls * TCH + c) * 1024, base + (KCH + VCH + c) * 1024, dlane);
 #pragma unroll
     for (int c = 0; c < FCH; ++c)
-      dma_x4(rf, (ls * FCH + c) * 1024, base + (KCH + VCH + TCH + c) * 1024, 16 * lane);
+      dma_x4(rf, (ls * FCH + c) * 1024, base + (KCH + VCH + TCH + c) * 1024, dlane);
     dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
   };
 
@@ -664,19 +684,19 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
-      load_k_tile<DP>(kb, kt, j, g, kr[kt]);
-      if constexpr (CW > 0) load_k_tile<GW>(vb, kt, j, g, vr[kt]);
+      load_k_tile_lds<DP>(kb, kt, j, g, kr[kt]);
+      if constexpr (CW > 0) load_k_tile_lds<GW>(vb, kt, j, g, vr[kt]);
     }
     // per key slot of this lane's B operand: sign(v_n) (single channel) or 1
     const uint4 sg = CW > 0 ? uint4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u}
                             : *reinterpret_cast<const uint4*>(sc + 32 + 4 * g);
     uint4 ktr[DT];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + j) * 4 + g];
+    for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + j) * 4 + lds_col(j, g)];
     uint4 vtr[FCH > 0 ? FCH : 1];
     const uint4* fb = reinterpret_cast<const uint4*>(base + (KCH + VCH + TCH) * 1024);
 #pragma unroll
-    for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + j) * 4 + g];
+    for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + j) * 4 + lds_col(j, g)];
     if constexpr (CW == 0) {
       // single channel: the score MFMAs of all query tiles, then their
       // exponentials, then the contractions over keys, kept apart by
