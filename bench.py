@@ -931,16 +931,21 @@ def main():
     pairs = float(w.M) * float(w.N)
     value = pairs / (ms_per_step * 1e-3)
 
-    # dominant kernel: the gradient kernel when gradients are taken (with the
-    # forward sum fused into the dq launch by default), else the forward
-    # kernel; one launch processes M*N pairs.  With dk also taken the launches
-    # alternate dq (fused) and dk; the per-launch work is averaged.
+    # dominant kernel: the gradient kernel when gradients are taken, else the
+    # forward kernel; one launch processes M*N pairs.  The library fuses a
+    # forward-type sum into a gradient launch (the forward into the dq pass,
+    # dv into the dk pass) for C = 1, or C <= 16 and D <= 128; otherwise that
+    # sum runs as a forward-kernel launch the gradient timing does not include.
+    # With dk also taken the launches alternate dq and dk; the per-launch work
+    # is averaged.
+    fusable = w.C == 1 or (w.C <= 16 and w.D <= 128)
+    fwd_in_dq = fused and fusable
     if any(grads):
         per_launch = []
         if grads[0]:
-            per_launch.append(4 * w.D + (4 if fused else 2) * w.C)
+            per_launch.append(4 * w.D + (4 if fwd_in_dq else 2) * w.C)
         if grads[1]:
-            per_launch.append(4 * w.D + 2 * w.C)
+            per_launch.append(4 * w.D + (4 if grads[2] and fusable else 2) * w.C)
         dom_flops = float(np.mean(per_launch)) * pairs
     else:
         dom_flops = (2 * w.D + 2 * w.C) * pairs
@@ -970,7 +975,7 @@ def main():
         "mfma_frac_of_peak": step_flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
         "roofline": {
             "bound": "mfma",
-            "kernel": ("k_dq (forward fused)" if fused else "k_dq") if any(grads) else "k_fwd",
+            "kernel": ("k_dq (forward fused)" if fwd_in_dq else "k_dq") if any(grads) else "k_fwd",
             "achieved": achieved,
             "peak": PEAK_MFMA_F16 / 1e12,
             "unit": "TFLOP/s",
