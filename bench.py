@@ -795,6 +795,9 @@ def main():
                          "Alg. 2 with autograd) beside the library")
     ap.add_argument("--batch-n", type=int, default=None, metavar="N",
                     help="--compare-attention on batch_grad_d32: M = N = this instead of 65536")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the step captured in a HIP graph and replayed (the kernel roofline "
+                         "still comes from the eager steps)")
     ap.add_argument("--peaks", action="store_true",
                     help="measure the device's MFMA, exp2, FMA and streaming-read rates and exit")
     ap.add_argument("--svgd-update", action="store_true",
@@ -880,18 +883,19 @@ def main():
     out = torch.empty((w.M, w.C), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
-    def step():
+    def step(on=None):
+        on = stream if on is None else on
         if args.flow:
-            gs.gauss_sum_mmd_flow(q, v, float(w.tau), workspace=ws, stream=stream)
+            gs.gauss_sum_mmd_flow(q, v, float(w.tau), workspace=ws, stream=on)
             return
         if fused:
             gs.gauss_sum_fwd_bwd(q, k, v, float(w.tau), g, want=grads, out=out, workspace=ws,
-                                 stream=stream)
+                                 stream=on)
             return
         if do_fwd:
-            gs.gauss_sum_fwd(q, k, v, float(w.tau), out=out, workspace=ws, stream=stream)
+            gs.gauss_sum_fwd(q, k, v, float(w.tau), out=out, workspace=ws, stream=on)
         if any(grads):
-            gs.gauss_sum_bwd(q, k, v, float(w.tau), g, want=grads, workspace=ws, stream=stream)
+            gs.gauss_sum_bwd(q, k, v, float(w.tau), g, want=grads, workspace=ws, stream=on)
 
     if args.calibrate_copy:
         nb = args.calibrate_copy * 1024 * 1024
@@ -928,6 +932,28 @@ def main():
     kernel_ms = gs.gauss_sum_profile_stop(cap)
     total_ms = e0.elapsed_time(e1)
     ms_per_step = total_ms / args.steps
+    eager_ms = ms_per_step
+    if args.graph:
+        # the same step captured once in a HIP graph and replayed: removes the
+        # per-launch host and queue costs that bound the small workloads
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step(side)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(torch.cuda.current_stream())
+        for _ in range(max(1, args.warmup)):
+            graph.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_per_step = e0.elapsed_time(e1) / args.steps
     pairs = float(w.M) * float(w.N)
     value = pairs / (ms_per_step * 1e-3)
 
@@ -971,7 +997,8 @@ def main():
                    "tau": float(w.tau), "passes": "+".join(passes),
                    "api": "gauss_sum_mmd_flow" if args.flow else "gauss_sum_fwd_bwd" if fused else
                           "+".join(n for n, u in (("gauss_sum_fwd", do_fwd),
-                                                  ("gauss_sum_bwd", any(grads))) if u)},
+                                                  ("gauss_sum_bwd", any(grads))) if u),
+                   "graph": bool(args.graph)},
         "mfma_frac_of_peak": step_flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
         "roofline": {
             "bound": "mfma",
@@ -988,6 +1015,8 @@ def main():
     }
     res["roofline"].update(measured_mfma(achieved))
     res["roofline"]["exp"] = exp_rate(pairs, avg_kernel_ms)
+    if args.graph:
+        res["eager_ms_per_step"] = eager_ms
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(w, passes, args.cpu_budget)
     print(json.dumps(res), flush=True)
