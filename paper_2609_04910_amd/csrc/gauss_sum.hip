@@ -544,7 +544,7 @@ inline unsigned grid1(int64_t n, int threads = 256) {
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(n, threads), 1 << 20));
 }
 // Reductions: at most 512 workgroups (grid-stride), one atomic each.
-inline unsigned grid_reduce(int64_t n) { return std::min(grid1(n), 512u); }
+inline unsigned grid_reduce(int64_t n) { return std::min(grid1(n), 128u); }
 
 // A launch group: G problems on grid.z, each with a workspace slice of
 // `slice` bytes (pl describes the first one).

@@ -47,6 +47,39 @@ __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
   uint32_t mb = 0;
+  auto take = [&](float f) {
+    const uint32_t b = __builtin_bit_cast(uint32_t, fabsf(f));
+    mb = b > mb ? b : mb;
+  };
+  if ((reinterpret_cast<uintptr_t>(x) & 15) == 0) {
+    // 16-byte loads (4 fp32 or 8 fp16 / bf16 elements), two in flight per
+    // thread; the tail of fewer than one vector's elements falls through
+    const int per = dtype == 0 ? 4 : 8;
+    const int64_t nv = count / per;
+    const uint4* xv = static_cast<const uint4*>(x);
+    auto vec = [&](const uint4 w) {
+      const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+      if (dtype == 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) take(__builtin_bit_cast(float, u[e]));
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint16_t lo = (uint16_t)(u[e] & 0xffffu), hi = (uint16_t)(u[e] >> 16);
+          take(dtype == 1 ? F16::to_float(lo) : BF16::to_float(lo));
+          take(dtype == 1 ? F16::to_float(hi) : BF16::to_float(hi));
+        }
+      }
+    };
+    int64_t j = i;
+    for (; j + stride < nv; j += 2 * stride) {
+      const uint4 a = xv[j], b = xv[j + stride];
+      vec(a);
+      vec(b);
+    }
+    for (; j < nv; j += stride) vec(xv[j]);
+    i = nv * per + i;  // scalar tail
+  }
   // four independent loads in flight per thread
   for (; i + 3 * stride < count; i += 4 * stride) {
     uint32_t b[4];
