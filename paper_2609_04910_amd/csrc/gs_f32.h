@@ -423,7 +423,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32c(
       load_k_tile_lds<DP>(khb, kt, j, g, khr);
       load_k_tile_lds<DP>(klb, kt, j, g, klr);
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score(khr, klr, qt, cin)));
+      for (int qt = 0; qt < QT; ++qt) smax[qt] = max_into(smax[qt], score(khr, klr, qt, cin));
     }
   };
   key_stream<NS, 2 * KCH + 1>(s_begin, s_end, issue_k, compute_max);

@@ -149,6 +149,11 @@ constexpr int ring_stages(int stage_bytes, int loads) {
 __device__ __forceinline__ float max4(floatx4 a) {
   return fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3]));
 }
+// Running maximum m folded with the four values of a, as a chain the compiler
+// turns into two three-operand maxima (v_max3_f32) instead of four maxima.
+__device__ __forceinline__ float max_into(float m, floatx4 a) {
+  return fmaxf(fmaxf(fmaxf(fmaxf(m, a[0]), a[1]), a[2]), a[3]);
+}
 
 __device__ __forceinline__ float wave_max_over_g(float x) {
   x = fmaxf(x, __shfl_xor(x, 16, kWave));
@@ -210,7 +215,7 @@ __device__ __forceinline__ bool needs_shift(const uint4* __restrict__ sample_rt,
     load_k_tile<DP>(sample_rt, t, j, g, kr);
     const floatx4 cin = *reinterpret_cast<const floatx4*>(sample_nh + 16 * t + 4 * g);
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
+    for (int qt = 0; qt < QT; ++qt) smax[qt] = max_into(smax[qt], score_tile<T, DP>(kr, qreg[qt], cin));
   }
   bool low = false;
 #pragma unroll
@@ -258,7 +263,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_row_check(
       load_k_tile<DP>(sample_rt, t, j, g, kr);
       const floatx4 cin = *reinterpret_cast<const floatx4*>(sample_nh + 16 * t + 4 * g);
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
+      for (int qt = 0; qt < QT; ++qt) smax[qt] = max_into(smax[qt], score_tile<T, DP>(kr, qreg[qt], cin));
     }
   };
   uint32_t level[QT];
@@ -316,7 +321,7 @@ __device__ __forceinline__ void exact_offsets(const uint4* __restrict__ ks, cons
           *reinterpret_cast<const floatx4*>(scal + (int64_t)s * kScalarFloats + 16 * kt + 4 * g);
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt)
-        smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
+        smax[qt] = max_into(smax[qt], score_tile<T, DP>(kr, qreg[qt], cin));
     }
   }
 #pragma unroll
@@ -473,7 +478,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
         uint4 kr[DP];
         load_k_tile_lds<DP>(kb, kt, j, g, kr);
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt) smax[qt] = fmaxf(smax[qt], max4(score_tile<T, DP>(kr, qreg[qt], cin)));
+        for (int qt = 0; qt < QT; ++qt) smax[qt] = max_into(smax[qt], score_tile<T, DP>(kr, qreg[qt], cin));
       }
     });
     __syncthreads();  // every wave is done with the ring before the main stream refills it
