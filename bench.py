@@ -1009,6 +1009,7 @@ def main():
             "frac": achieved / (PEAK_MFMA_F16 / 1e12),
             "traffic": recorded_traffic(args.workload, "k_dq" if any(grads) else "k_fwd"),
             "avg_launch_ms": avg_kernel_ms,
+            "std_launch_ms": float(np.std(kernel_ms)) if kernel_ms else float("nan"),
             "launches": len(kernel_ms),
             "flops_per_launch": dom_flops,
         },
