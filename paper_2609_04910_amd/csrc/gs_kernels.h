@@ -516,6 +516,35 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     const uint4* vb = reinterpret_cast<const uint4*>(base + KCH * 1024);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) vr[ct] = vb[(16 * ct + j) * 4 + lds_col(j, g)];
+    if constexpr (DP == 1 && CT == 1) {
+      // one 32-wide chunk and one value tile: all score MFMAs of the step,
+      // then the exponentials, then the value contractions, kept apart by
+      // scheduling barriers (3 % faster than tile by tile at D = 32 although
+      // the accumulators cost one wave per SIMD)
+      floatx4 acc[QT][2];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) acc[qt][kt] = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
+      __builtin_amdgcn_sched_barrier(0);
+      uint4 b[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        float p[2][4];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float y = fmaf(acc[qt][kt][r], tau2, bq[qt]);
+            p[kt][r] = SH ? exp2_shifted(y) : exp2_clamped(y);
+          }
+        b[qt] = pack_tile_pair(p);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) O[qt][0] = mfma_f16(vr[0], b[qt], O[qt][0]);
+      return;
+    }
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       float p[2][4];
