@@ -1,17 +1,21 @@
 """Benchmark: exact Gauss-sum pair interactions per second on one MI355X.
 
 Default workload (one "step" = the whole hot path over one batch):
-  mmd_flow -- MMD-gradient-flow shape, M = N = 65536 points in 64-D (two
-  Gaussian clouds, means 0 and 0.5*1, fp16), signed two-sample weights
-  v = +-1/N (C = 1), tau = 1/median squared pairwise distance; a step is the
-  forward sum s = sum_n Phi v_n plus its query gradient dq (upstream gradient
-  g = v), i.e. what one MMD-flow iteration evaluates.  By default a step is
-  one gauss_sum_fwd_bwd call (the forward and dq from one pass over the pairs);
-  --separate times gauss_sum_fwd followed by gauss_sum_bwd instead.
+  rect_d256 -- M = 2^17 queries against N = 2^21 keys in 256-D (independent
+  unit-normalised Gaussian vectors, fp16), C = 16 signed values (10 % zero
+  rows), tau = 4; a step is the forward sum s and the gradients dq, dk, dv
+  of sum(dout * s) for dout ~ N(0, 1): one gauss_sum_fwd_bwd call.  It is the
+  largest configuration and the one that runs the forward and all three
+  gradients.  The same JSON line carries compact records of the other
+  configurations (dense_d16 -- also timed as 1000 back-to-back calls per
+  event pair and as single calls --, mmd_flow, svgd, mixture_d32 at
+  tau = 0.1, 1, 10); --no-configs leaves them out.
 
-Other workloads (--workload) use the same JSON format: dense_d16 (forward),
-svgd (forward + dq, dk, dv), mixture_d32 (forward, --tau), rect_d256
-(forward + dq, dk, dv).
+Other workloads (--workload) print one line of the same format for that
+workload alone: dense_d16 (forward), mmd_flow (forward + dq, fused; --flow
+times gauss_sum_mmd_flow, --separate gauss_sum_fwd + gauss_sum_bwd), svgd
+(forward + dq, dk, dv), mixture_d32 (forward, --tau), and the batched
+layouts of Sec. 4.
 
 Protocol: inputs are generated on the host (seeded), copied to HBM before
 timing.  The step is first repeated, untimed, for --settle-ms of wall time:
@@ -35,6 +39,7 @@ Prints one JSON line.
 """
 import argparse
 import csv
+import ctypes
 import glob
 import hashlib
 import json
@@ -79,6 +84,23 @@ def flops_per_pair(passes, D, C, fused):
             f += 2 * D + 2 * C
         else:  # dq or dk
             f += 4 * D + 2 * C
+    return f
+
+
+def algorithmic_flops_per_pair(passes, D, C):
+    """The step's algorithmic flops per pair, independent of how the library
+    splits it into launches: the forward 2D+2C (q.k and the value
+    contraction); the backward 2D for its own q.k, 2C for <g, v> (dq or dk),
+    2D each for the sums of P k (dq) and P q (dk), 2C for dv -- the full
+    backward 6D+4C, so forward plus full backward is 8D+6C.  With dq the
+    only gradient the forward and dq are one pass over the same q.k tiles,
+    counted once: 4D+4C."""
+    dq, dk, dv, fwd = "dq" in passes, "dk" in passes, "dv" in passes, "fwd" in passes
+    f = 2 * D + 2 * C if fwd else 0
+    if dq or dk or dv:
+        f += 2 * D + (2 * C if (dq or dk) else 0) + 2 * D * dq + 2 * D * dk + 2 * C * dv
+        if fwd and dq and not dk and not dv:
+            f -= 2 * D
     return f
 
 
@@ -199,8 +221,7 @@ def cpu_baseline(w, passes, budget_s=15.0):
 
     import oracle
 
-    threads = oracle.default_threads()
-    threads = min(threads, 16)
+    threads = oracle.default_threads()   # every host core this process may run on
     g = w.g
     if g is None and any(p != "fwd" for p in passes):
         g = np.random.default_rng(99).standard_normal((w.M, w.C)).astype(np.float32)
@@ -248,11 +269,320 @@ def cpu_baseline(w, passes, budget_s=15.0):
         "value": pairs / t,
         "unit": "pairs/s",
         "cores": threads,
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": "fp64 oracle, passes %s on %d of %d query rows%s, each against all partners, %.1f s"
                   % ("+".join(passes), nq2 if has_q else 0, w.M,
                      (" and %d of %d key rows" % (nk2, w.N)) if has_k else "", t),
+        # the whole step (all M x N pairs of every pass) at the sampled rate
+        "full_problem_s_extrapolated": w.M * float(w.N) / (pairs / t),
     }
+
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def fused_passes(D, C):
+    """Which forward-type sums the library computes inside a gradient launch
+    (the fusion rule of gauss_sum_fwd_bwd): (forward inside the dq pass, dv
+    inside the dk pass)."""
+    f = C == 1 or (C <= 16 and D <= 128)
+    return f, f
+
+
+def dominant_flops(passes, D, C, fused_call):
+    """Algorithmic flops per pair of one launch of the dominant kernel: a
+    gradient launch (dq or dk, averaged over the gradient launches of a step)
+    when gradients are taken, else the forward launch."""
+    fwd_in_dq, dv_in_dk = fused_passes(D, C)
+    per_launch = []
+    if "dq" in passes:
+        per_launch.append(4 * D + (4 if (fused_call and "fwd" in passes and fwd_in_dq) else 2) * C)
+    if "dk" in passes:
+        per_launch.append(4 * D + (4 if ("dv" in passes and dv_in_dk) else 2) * C)
+    if per_launch:
+        return sum(per_launch) / len(per_launch)
+    return 2 * D + 2 * C
+
+
+def clean(res):
+    """The result without the private (underscore) entries."""
+    return {k: v for k, v in res.items() if not k.startswith("_")}
+
+
+def measure_workload(args, name, tau, steps, warmup, settle_ms, graph=False, flow=False, separate=False,
+                     calibrate_copy=0, calls_per_pair=0):
+    """Times `steps` steps of workload `name` on cuda:0 (inputs resident in
+    HBM; untimed settle and warm-up first) and returns the benchmark record:
+    pairs/s, ms per step, the dominant kernel's roofline from the library's
+    HIP-event hook.  calls_per_pair > 0 also times that many back-to-back
+    steps between one pair of events and single steps one at a time (the
+    launch-latency floor of the smallest problem)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_04910_amd import gauss_sum as gs
+    from paper_2609_04910_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    passes = PASSES[name]
+    w = wl.make(name, seed=0, tau=tau)
+    if w.g is None and any(p != "fwd" for p in passes):
+        w.g = np.random.default_rng(99).standard_normal((w.M, w.C)).astype(np.float32)
+
+    def t(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    q = t(w.q)
+    k = q if w.same_points else t(w.k)
+    v = t(w.v)
+    g = t(w.g) if w.g is not None else None
+    grads = tuple(p in passes for p in ("dq", "dk", "dv"))
+    do_fwd = "fwd" in passes
+    if flow and name != "mmd_flow":
+        print("--flow applies to the mmd_flow workload only", file=sys.stderr)
+        sys.exit(2)
+    fused = do_fwd and any(grads) and not separate
+    qk_code = gs.GS_F16 if w.qk_dtype == "f16" else gs.GS_BF16
+    v_code = {np.dtype(np.float32): gs.GS_F32, np.dtype(np.float16): gs.GS_F16}[w.v.dtype]
+    ws_f = gs.gauss_sum_fwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code) if do_fwd else 0
+    ws_b = gs.gauss_sum_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if any(grads) else 0
+    ws_fb = gs.gauss_sum_fwd_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if fused else 0
+    ws_fl = gs.gauss_sum_mmd_flow_workspace_size(w.N, w.D, qk_code, v_code) if flow else 0
+    ws = torch.empty(max(ws_f, ws_b, ws_fb, ws_fl, 1), dtype=torch.uint8, device=dev)
+    out = torch.empty((w.M, w.C), dtype=torch.float32, device=dev)
+    dq = torch.empty((w.M, w.D), dtype=torch.float32, device=dev) if grads[0] else None
+    dk = torch.empty((w.N, w.D), dtype=torch.float32, device=dev) if grads[1] else None
+    dv = torch.empty((w.N, w.C), dtype=torch.float32, device=dev) if grads[2] else None
+    stream = torch.cuda.current_stream()
+    lib = gs.load()
+    prob = gs.make_problem(w.M, w.N, w.D, w.C, qk_code, v_code)
+    g_code = gs.GS_F32 if g is None else gs._dtype_code(g.dtype)
+    nbytes = ws.numel()
+    P = gs._ptr
+
+    # the step calls the C ABI directly (outputs and workspace preallocated),
+    # so the timed region holds library work only
+    def step(on=None):
+        s_ = (stream if on is None else on).cuda_stream
+        if flow:
+            gs.gauss_sum_mmd_flow(q, v, float(w.tau), workspace=ws, stream=stream if on is None else on)
+            return
+        if fused:
+            st = lib.gauss_sum_fwd_bwd(ctypes.byref(prob), P(q), P(k), P(v), float(w.tau), P(g), g_code,
+                                       P(out), P(dq), P(dk), P(dv), P(ws), nbytes, ctypes.c_void_p(s_))
+        else:
+            st = 0
+            if do_fwd:
+                st = lib.gauss_sum_fwd(ctypes.byref(prob), P(q), P(k), P(v), float(w.tau), P(out), P(ws), nbytes,
+                                       ctypes.c_void_p(s_))
+            if any(grads) and st == 0:
+                st = lib.gauss_sum_bwd(ctypes.byref(prob), P(q), P(k), P(v), float(w.tau), P(g), g_code, P(dq),
+                                       P(dk), P(dv), P(ws), nbytes, ctypes.c_void_p(s_))
+        if st != 0:
+            raise gs.GaussSumError(st, "benchmark step")
+
+    if calibrate_copy:
+        nb = calibrate_copy * 1024 * 1024
+        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    settle_steps = 0
+    t_settle = time.perf_counter()
+    while settle_steps == 0 or (time.perf_counter() - t_settle) * 1e3 < settle_ms:
+        step()
+        settle_steps += 1
+        torch.cuda.synchronize()
+    settle_ms_done = (time.perf_counter() - t_settle) * 1e3
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+
+    kind = gs.PROFILE_GRAD if any(grads) else gs.PROFILE_FWD
+    launches_per_step = sum(grads[:2]) if any(grads) else 1
+    cap = steps * max(1, launches_per_step)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    gs.gauss_sum_profile_start(cap, kind)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    kernel_ms = gs.gauss_sum_profile_stop(cap)
+    ms_per_step = e0.elapsed_time(e1) / steps
+    eager_ms = ms_per_step
+    extra = {}
+    if calls_per_pair:
+        e0.record(stream)
+        for _ in range(calls_per_pair):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        extra["ms_per_call_back_to_back"] = e0.elapsed_time(e1) / calls_per_pair
+        extra["calls_per_event_pair"] = calls_per_pair
+        single = []
+        for _ in range(20):
+            torch.cuda.synchronize()
+            e0.record(stream)
+            step()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            single.append(e0.elapsed_time(e1))
+        extra["ms_single_call_median"] = float(np.median(single))
+        ms_per_step = extra["ms_per_call_back_to_back"]
+    if graph:
+        # the same step captured once in a HIP graph and replayed
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step(side)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        cg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(cg):
+            step(torch.cuda.current_stream())
+        for _ in range(max(1, warmup)):
+            cg.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            cg.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_per_step = e0.elapsed_time(e1) / steps
+    pairs = float(w.M) * float(w.N)
+    value = pairs / (ms_per_step * 1e-3)
+
+    # dominant kernel: the gradient kernel when gradients are taken, else the
+    # forward kernel; one launch processes M*N pairs
+    fwd_in_dq, _ = fused_passes(w.D, w.C)
+    dom_flops = dominant_flops(passes, w.D, w.C, fused) * pairs
+    avg_kernel_ms = float(np.mean(kernel_ms)) if kernel_ms else float("nan")
+    achieved = dom_flops / (avg_kernel_ms * 1e-3) / 1e12
+    step_flops = flops_per_pair(passes, w.D, w.C, fused) * pairs
+    alg_flops = algorithmic_flops_per_pair(passes, w.D, w.C) * pairs
+
+    res = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "settle": {"ms": settle_ms_done, "steps": settle_steps},
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if w.qk_dtype == "f16" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": describe(w, passes), "M": w.M, "N": w.N, "D": w.D, "C": w.C,
+                   "tau": float(w.tau), "passes": "+".join(passes),
+                   "api": "gauss_sum_mmd_flow" if flow else "gauss_sum_fwd_bwd" if fused else
+                          "+".join(n for n, u in (("gauss_sum_fwd", do_fwd),
+                                                  ("gauss_sum_bwd", any(grads))) if u),
+                   "graph": bool(graph)},
+        "mfma_frac_of_peak": step_flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
+        "step_roofline": {"flops_per_pair": algorithmic_flops_per_pair(passes, w.D, w.C),
+                          "basis": "algorithmic flops per pair of the step (forward 2D+2C, full "
+                                   "backward 6D+4C; fwd+dq 4D+4C) over the step time",
+                          "achieved": alg_flops / (ms_per_step * 1e-3) / 1e12, "unit": "TFLOP/s",
+                          "peak": PEAK_MFMA_F16 / 1e12,
+                          "frac": alg_flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": ("k_dq (forward fused)" if (fused and fwd_in_dq) else "k_dq") if any(grads) else "k_fwd",
+            "achieved": achieved,
+            "peak": PEAK_MFMA_F16 / 1e12,
+            "unit": "TFLOP/s",
+            "frac": achieved / (PEAK_MFMA_F16 / 1e12),
+            "traffic": recorded_traffic(name, "k_dq" if any(grads) else "k_fwd"),
+            "avg_launch_ms": avg_kernel_ms,
+            "std_launch_ms": float(np.std(kernel_ms)) if kernel_ms else float("nan"),
+            "launches": len(kernel_ms),
+            "flops_per_launch": dom_flops,
+        },
+    }
+    res["roofline"].update(measured_mfma(achieved))
+    res["roofline"]["exp"] = exp_rate(pairs, avg_kernel_ms)
+    res.update(extra)
+    if graph:
+        res["eager_ms_per_step"] = eager_ms
+    res["_workload"] = w
+    res["_passes"] = passes
+    del q, k, v, g, ws, out, dq, dk, dv
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def sub_record(res, tau=None):
+    """The compact form of a workload's record that the headline line carries."""
+    pk = measured_peaks()
+    c = res["config"]
+    pairs = float(c["M"]) * c["N"]
+    out = {"workload": c["workload"].split(":")[0], "M": c["M"], "N": c["N"], "D": c["D"], "C": c["C"],
+           "tau": c["tau"], "passes": c["passes"], "api": c["api"], "steps": res["steps"],
+           "ms_per_step": res["ms_per_step"], "pairs_per_s": res["value"],
+           "step_frac_of_mfma_peak": res["step_roofline"]["frac"],
+           "kernel": res["roofline"]["kernel"], "avg_launch_ms": res["roofline"]["avg_launch_ms"],
+           "kernel_frac_of_mfma_peak": res["roofline"]["frac"]}
+    if c["D"] <= 32:
+        # one exponential per pair and pass: the target for D <= 32 is stated
+        # against the exponential rate
+        out["exp_per_s_step"] = pairs * len(c["passes"].split("+")) / (res["ms_per_step"] * 1e-3)
+        out["exp_per_s_kernel"] = res["roofline"]["exp"]["achieved"]
+        if pk:
+            out["step_frac_of_measured_exp_rate"] = out["exp_per_s_step"] / pk["exp2_per_s"]
+            out["kernel_frac_of_measured_exp_rate"] = out["exp_per_s_kernel"] / pk["exp2_per_s"]
+    for key in ("ms_per_call_back_to_back", "calls_per_event_pair", "ms_single_call_median"):
+        if key in res:
+            out[key] = res[key]
+    return out
+
+
+def bench_headline(args):
+    """The benchmark line: rect_d256 (the largest configuration, forward and
+    all three gradients) as the headline, with compact records of the other
+    configurations (dense_d16 with back-to-back and single calls, mmd_flow,
+    svgd, mixture_d32 at each tau) in the same JSON line."""
+    import torch
+
+    configs = []
+    if not args.no_configs:
+        for name, tau, steps in (("dense_d16", None, 20), ("mmd_flow", None, 20), ("svgd", None, 20),
+                                 ("mixture_d32", 0.1, 5), ("mixture_d32", 1.0, 5), ("mixture_d32", 10.0, 5)):
+            print("config", name, tau, flush=True, file=sys.stderr)
+            r = measure_workload(args, name, tau, steps, 2, 200.0,
+                                 calls_per_pair=1000 if name == "dense_d16" else 0)
+            configs.append(sub_record(r))
+            del r
+            torch.cuda.empty_cache()
+    print("headline rect_d256", flush=True, file=sys.stderr)
+    res = measure_workload(args, "rect_d256", None, args.steps, args.warmup, args.settle_ms,
+                           calibrate_copy=args.calibrate_copy)
+    if configs:
+        res["configs"] = configs
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(res.pop("_workload"), res.pop("_passes"), args.cpu_budget)
+    print(json.dumps(clean(res)), flush=True)
 
 
 def bench_batched(args):
@@ -336,7 +666,7 @@ def bench_batched(args):
         res["roofline"].update(measured_mfma(achieved))
     res["roofline"]["exp"] = exp_rate(float(B) / per_step * M * N, avg)
     if not args.no_cpu:
-        threads = min(oracle.default_threads(), 16)
+        threads = oracle.default_threads()
         oracle.fwd(q[0], k[0], v[0], float(tau), rows=np.arange(1), threads=threads)
         # whole problems (every query row against every key), in order, until
         # the time budget is spent
@@ -431,7 +761,7 @@ def bench_batched_grad(args):
     # two passes over every pair per step (dq, dk), one exponential each
     res["roofline"]["exp"] = exp_rate(2.0 * pairs / per_step, grad_ms / per_step)
     if not args.no_cpu:
-        threads = min(oracle.default_threads(), 16)
+        threads = oracle.default_threads()
         rows = wl.sample_rows(M, 64, seed=5)
         oracle.dq(q[0], k[0], v[0], g[0], float(tau), rows=rows[:1], threads=threads)
         t0, done = time.perf_counter(), 0
@@ -782,9 +1112,11 @@ def main():
                     help="also run a device copy of MIB MiB (counter calibration for --traffic-from)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="record roofline traffic from two rocprofv3 --pmc csv outputs and exit")
-    ap.add_argument("--workload", default="mmd_flow", choices=sorted(PASSES) + ["batch_d32", "batch_d32_f32", "batch_c32", "batch_c32_f32", "batch_grad_d32"])
+    ap.add_argument("--workload", default="rect_d256", choices=sorted(PASSES) + ["batch_d32", "batch_d32_f32", "batch_c32", "batch_c32_f32", "batch_grad_d32"])
     ap.add_argument("--tau", type=float, default=None, help="mixture_d32 bandwidth (0.1, 1, 10)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="rect_d256: time the headline workload only (no records of the other configurations)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--flow", action="store_true",
                     help="mmd_flow: time one gauss_sum_mmd_flow call per step (s, the flow field "
@@ -852,176 +1184,15 @@ def main():
             bench_batched(args)
         return
 
-    passes = PASSES[args.workload]
-    tau = args.tau if args.workload == "mixture_d32" else None
-    w = wl.make(args.workload, seed=0, tau=tau)
-    if w.g is None and any(p != "fwd" for p in passes):
-        w.g = np.random.default_rng(99).standard_normal((w.M, w.C)).astype(np.float32)
-
-    def t(a):
-        if a.dtype == np.uint16:
-            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
-        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-
-    q = t(w.q)
-    k = q if w.same_points else t(w.k)
-    v = t(w.v)
-    g = t(w.g) if w.g is not None else None
-    grads = tuple(p in passes for p in ("dq", "dk", "dv"))
-    do_fwd = "fwd" in passes
-    if args.flow and args.workload != "mmd_flow":
-        print("--flow applies to the mmd_flow workload only", file=sys.stderr)
-        sys.exit(2)
-    fused = do_fwd and any(grads) and not args.separate
-    qk_code = gs.GS_F16 if w.qk_dtype == "f16" else gs.GS_BF16
-    v_code = {np.dtype(np.float32): gs.GS_F32, np.dtype(np.float16): gs.GS_F16}[w.v.dtype]
-    ws_f = gs.gauss_sum_fwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code) if do_fwd else 0
-    ws_b = gs.gauss_sum_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if any(grads) else 0
-    ws_fb = gs.gauss_sum_fwd_bwd_workspace_size(w.M, w.N, w.D, w.C, qk_code, v_code, *grads) if fused else 0
-    ws_fl = gs.gauss_sum_mmd_flow_workspace_size(w.N, w.D, qk_code, v_code) if args.flow else 0
-    ws = torch.empty(max(ws_f, ws_b, ws_fb, ws_fl, 1), dtype=torch.uint8, device=dev)
-    out = torch.empty((w.M, w.C), dtype=torch.float32, device=dev)
-    stream = torch.cuda.current_stream()
-
-    def step(on=None):
-        on = stream if on is None else on
-        if args.flow:
-            gs.gauss_sum_mmd_flow(q, v, float(w.tau), workspace=ws, stream=on)
-            return
-        if fused:
-            gs.gauss_sum_fwd_bwd(q, k, v, float(w.tau), g, want=grads, out=out, workspace=ws,
-                                 stream=on)
-            return
-        if do_fwd:
-            gs.gauss_sum_fwd(q, k, v, float(w.tau), out=out, workspace=ws, stream=on)
-        if any(grads):
-            gs.gauss_sum_bwd(q, k, v, float(w.tau), g, want=grads, workspace=ws, stream=on)
-
-    if args.calibrate_copy:
-        nb = args.calibrate_copy * 1024 * 1024
-        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    settle_steps = 0
-    t_settle = time.perf_counter()
-    while settle_steps == 0 or (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
-        step()
-        settle_steps += 1
-        torch.cuda.synchronize()
-    settle_ms = (time.perf_counter() - t_settle) * 1e3
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    kind = gs.PROFILE_GRAD if any(grads) else gs.PROFILE_FWD
-    launches_per_step = sum(grads[:2]) if any(grads) else 1
-    cap = args.steps * max(1, launches_per_step)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    gs.gauss_sum_profile_start(cap, kind)
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    kernel_ms = gs.gauss_sum_profile_stop(cap)
-    total_ms = e0.elapsed_time(e1)
-    ms_per_step = total_ms / args.steps
-    eager_ms = ms_per_step
-    if args.graph:
-        # the same step captured once in a HIP graph and replayed: removes the
-        # per-launch host and queue costs that bound the small workloads
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        with torch.cuda.stream(side):
-            step(side)
-        stream.wait_stream(side)
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            step(torch.cuda.current_stream())
-        for _ in range(max(1, args.warmup)):
-            graph.replay()
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(args.steps):
-            graph.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms_per_step = e0.elapsed_time(e1) / args.steps
-    pairs = float(w.M) * float(w.N)
-    value = pairs / (ms_per_step * 1e-3)
-
-    # dominant kernel: the gradient kernel when gradients are taken, else the
-    # forward kernel; one launch processes M*N pairs.  The library fuses a
-    # forward-type sum into a gradient launch (the forward into the dq pass,
-    # dv into the dk pass) for C = 1, or C <= 16 and D <= 128; otherwise that
-    # sum runs as a forward-kernel launch the gradient timing does not include.
-    # With dk also taken the launches alternate dq and dk; the per-launch work
-    # is averaged.
-    fusable = w.C == 1 or (w.C <= 16 and w.D <= 128)
-    fwd_in_dq = fused and fusable
-    if any(grads):
-        per_launch = []
-        if grads[0]:
-            per_launch.append(4 * w.D + (4 if fwd_in_dq else 2) * w.C)
-        if grads[1]:
-            per_launch.append(4 * w.D + (4 if grads[2] and fusable else 2) * w.C)
-        dom_flops = float(np.mean(per_launch)) * pairs
-    else:
-        dom_flops = (2 * w.D + 2 * w.C) * pairs
-    avg_kernel_ms = float(np.mean(kernel_ms)) if kernel_ms else float("nan")
-    achieved = dom_flops / (avg_kernel_ms * 1e-3) / 1e12
-    step_flops = flops_per_pair(passes, w.D, w.C, fused) * pairs
-
-    res = {
-        "metric": METRIC,
-        "value": value,
-        "unit": "pairs/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "settle": {"ms": settle_ms, "steps": settle_steps},
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f16" if w.qk_dtype == "f16" else "bf16",
-        "data": "synthetic",
-        "config": {"workload": describe(w, passes), "M": w.M, "N": w.N, "D": w.D, "C": w.C,
-                   "tau": float(w.tau), "passes": "+".join(passes),
-                   "api": "gauss_sum_mmd_flow" if args.flow else "gauss_sum_fwd_bwd" if fused else
-                          "+".join(n for n, u in (("gauss_sum_fwd", do_fwd),
-                                                  ("gauss_sum_bwd", any(grads))) if u),
-                   "graph": bool(args.graph)},
-        "mfma_frac_of_peak": step_flops / (ms_per_step * 1e-3) / PEAK_MFMA_F16,
-        "roofline": {
-            "bound": "mfma",
-            "kernel": ("k_dq (forward fused)" if fwd_in_dq else "k_dq") if any(grads) else "k_fwd",
-            "achieved": achieved,
-            "peak": PEAK_MFMA_F16 / 1e12,
-            "unit": "TFLOP/s",
-            "frac": achieved / (PEAK_MFMA_F16 / 1e12),
-            "traffic": recorded_traffic(args.workload, "k_dq" if any(grads) else "k_fwd"),
-            "avg_launch_ms": avg_kernel_ms,
-            "std_launch_ms": float(np.std(kernel_ms)) if kernel_ms else float("nan"),
-            "launches": len(kernel_ms),
-            "flops_per_launch": dom_flops,
-        },
-    }
-    res["roofline"].update(measured_mfma(achieved))
-    res["roofline"]["exp"] = exp_rate(pairs, avg_kernel_ms)
-    if args.graph:
-        res["eager_ms_per_step"] = eager_ms
+    if args.workload == "rect_d256" and not args.no_configs and not (args.flow or args.graph or args.separate):
+        bench_headline(args)
+        return
+    res = measure_workload(args, args.workload, args.tau if args.workload == "mixture_d32" else None,
+                           args.steps, args.warmup, args.settle_ms, graph=args.graph, flow=args.flow,
+                           separate=args.separate, calibrate_copy=args.calibrate_copy)
     if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline(w, passes, args.cpu_budget)
-    print(json.dumps(res), flush=True)
-
+        res["cpu_baseline"] = cpu_baseline(res.pop("_workload"), res.pop("_passes"), args.cpu_budget)
+    print(json.dumps(clean(res)), flush=True)
 
 if __name__ == "__main__":
     main()

@@ -8,7 +8,9 @@
  *   - the transcendental rate of v_exp_f32 (independent chains of exp2; the
  *     Gauss sum evaluates one exponential per (query, key) pair, Eq. 1),
  *   - the fp32 FMA rate of the vector ALU (unpacked, as the library builds it),
- *   - the streaming read bandwidth of device memory.
+ *   - the streaming read bandwidth of device memory,
+ *   - the read bandwidth of the local data share (ds_read_b128 on linear
+ *     addresses; the main kernels read their MFMA operands from LDS).
  *
  * Every kernel runs `workgroups` workgroups of GS_PEAKS_THREADS threads and
  * writes one 32-bit value per thread to `out` (so the work cannot be removed
@@ -21,6 +23,8 @@
  *   exp:   workgroups * GS_PEAKS_THREADS * iters * GS_PEAKS_CHAINS exp2
  *   fma:   workgroups * GS_PEAKS_THREADS * iters * GS_PEAKS_CHAINS fma (2 flop each)
  *   read:  `bytes` bytes of `in`, read once
+ *   lds:   workgroups * GS_PEAKS_THREADS * iters * GS_PEAKS_LDS_READS * 16 bytes
+ *          read from LDS (each workgroup first fills 32 KiB of LDS)
  * All calls are asynchronous on `stream`; arguments are checked before the
  * launch.  Return value: 0 on success, 1 for an invalid argument (NULL
  * pointer, non-positive size, `bytes` not a multiple of 16, `in` not 16-byte
@@ -40,11 +44,13 @@ extern "C" {
 #define GS_PEAKS_THREADS 256
 #define GS_PEAKS_MFMA_CHAINS 4
 #define GS_PEAKS_CHAINS 8
+#define GS_PEAKS_LDS_READS 4
 
 int gs_peaks_mfma(float* out, int64_t workgroups, int32_t iters, int32_t shape, hipStream_t stream);
 int gs_peaks_exp(float* out, int64_t workgroups, int32_t iters, hipStream_t stream);
 int gs_peaks_fma(float* out, int64_t workgroups, int32_t iters, hipStream_t stream);
 int gs_peaks_read(const void* in, int64_t bytes, uint32_t* out, int64_t workgroups, hipStream_t stream);
+int gs_peaks_lds(uint32_t* out, int64_t workgroups, int32_t iters, hipStream_t stream);
 
 #ifdef __cplusplus
 }

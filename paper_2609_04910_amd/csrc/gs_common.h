@@ -92,6 +92,34 @@ __device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, halfx2));
 }
 
+// Register fences for operands loaded from global memory before a key loop.
+// The direct HBM -> LDS copies of the loops are inline assembly, which the
+// compiler does not count in its memory-counter bookkeeping: if the first
+// use of a prologue load sits inside the loop, the compiler's wait for it
+// there ("at most n loads outstanding", n counting only its own loads)
+// executes on every step and also waits for most of the step's own
+// prefetch.  An empty assembly statement that reads and writes the register
+// is such a use, placed before the loop, so the wait happens there once.
+__device__ __forceinline__ void settle(float& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void settle(uint4& x) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 t = __builtin_bit_cast(u32x4, x);
+  asm volatile("" : "+v"(t));
+  x = __builtin_bit_cast(uint4, t);
+}
+template <typename T, int A, int B>
+__device__ __forceinline__ void settle(T (&x)[A][B]) {
+#pragma unroll
+  for (int a = 0; a < A; ++a)
+#pragma unroll
+    for (int b = 0; b < B; ++b) settle(x[a][b]);
+}
+template <typename T, int A>
+__device__ __forceinline__ void settle(T (&x)[A]) {
+#pragma unroll
+  for (int a = 0; a < A; ++a) settle(x[a]);
+}
+
 // Element i of an fp32 / fp16 / bf16 array (dtype codes of gs_dtype: 0, 1, 2).
 __device__ __forceinline__ float load_any(const void* p, int64_t i, int dtype) {
   if (dtype == 0) return static_cast<const float*>(p)[i];

@@ -229,6 +229,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32(
     bq[qt] = tau2 * nhq[q0 + 16 * qt + j];
     A[qt] = Ac[qt] = blk[qt] = 0.0f;
   }
+  settle(qhr);
+  settle(qlr);
+  settle(bq);
   // Kahan: A + Ac carries the sum of the finished blocks
   auto close_block = [&]() {
 #pragma unroll
@@ -398,6 +401,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd32c(
     bq[qt] = tau2 * nhq[q0 + 16 * qt + j];
     smax[qt] = -__builtin_inff();
   }
+  settle(qhr);
+  settle(qlr);
+  settle(bq);
   auto score = [&](const uint4 (&khr)[DP], const uint4 (&klr)[DP], int qt, floatx4 cin) {
     floatx4 acc = cin;
 #pragma unroll

@@ -492,6 +492,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
     }
   }
 
+  settle(qreg);
+  settle(bq);
   floatx4 O[QT][CT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt)
@@ -693,6 +695,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
   }
   if (needs_shift<T, DP, QT>(samp_rt, samp_nh, qreg, bq, tau2, q0, M, j, g))
     exact_offsets<T, DP, QT>(ks, scal, qreg, s_begin, s_end, j, g, tau2, bq, off);
+  if constexpr (CW > 0) settle(greg);
 
   floatx4 dQ[QT][DT];
   float rs[QT];

@@ -187,13 +187,46 @@ def _ptr(t):
 
 
 def _check_inputs(q, k, v):
+    """q: M x D, k: N x D, v: N x C, contiguous, on one GPU; q and k share a
+    dtype.  Shapes are checked before devices (so a mismatch is reported the
+    same way on any machine)."""
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dim() != 2 or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous 2-d tensor" % name)
+    if tuple(k.shape) != (v.shape[0], q.shape[1]):
+        raise ValueError("k must be %d x %d (rows of v x columns of q), got %s"
+                         % (v.shape[0], q.shape[1], tuple(k.shape)))
+    if q.dtype != k.dtype:
+        raise TypeError("q and k must share a dtype")
     for name, t in (("q", q), ("k", k), ("v", v)):
         if not t.is_cuda:
             raise ValueError("%s must be a GPU tensor" % name)
-        if t.dim() != 2 or not t.is_contiguous():
-            raise ValueError("%s must be a contiguous 2-d tensor" % name)
-    if q.dtype != k.dtype:
-        raise TypeError("q and k must share a dtype")
+    if k.device != q.device or v.device != q.device:
+        raise ValueError("q, k and v must be on one device")
+
+
+def _check_tensor(t, name, shape, device, dtype=None):
+    """A caller-supplied tensor: the exact shape, contiguous (and of `dtype`
+    if given), on `device`."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a tensor" % name)
+    if tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous %s tensor, got %s" % (name, "x".join(map(str, shape)),
+                                                                      tuple(t.shape)))
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_cuda or t.device != device:
+        raise ValueError("%s must be a GPU tensor on %s" % (name, device))
+
+
+def _output(out, name, shape, device):
+    """`out` checked (fp32, exact shape, contiguous, on device), or a new one."""
+    import torch
+    if out is None:
+        return torch.empty(shape, dtype=torch.float32, device=device)
+    _check_tensor(out, name, shape, device, torch.float32)
+    return out
 
 
 def _workspace(nbytes, device):
@@ -203,10 +236,36 @@ def _workspace(nbytes, device):
     return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
 
 
-def _stream(stream):
+def _workspace_arg(workspace, need, device):
+    """(workspace tensor, its bytes): the caller's (contiguous, on device; the
+    library checks the size) or a new one of `need` bytes."""
+    if workspace is None:
+        return _workspace(need, device)
+    if not workspace.is_cuda or workspace.device != device or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous GPU tensor on %s" % device)
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def _stream_of(stream):
     import torch
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return ctypes.c_void_p(s.cuda_stream)
+    return stream if stream is not None else torch.cuda.current_stream()
+
+
+def _stream(stream):
+    return ctypes.c_void_p(_stream_of(stream).cuda_stream)
+
+
+def _keep_alive(stream, *tensors):
+    """Tensors allocated here on torch's current stream but used by kernels
+    enqueued on another `stream`: mark them as in use on that stream, so the
+    caching allocator does not hand their memory out again before those
+    kernels finish."""
+    import torch
+    if stream is None or stream == torch.cuda.current_stream():
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
 
 
 def gauss_sum_fwd(q, k, v, tau, out=None, workspace=None, stream=None):
@@ -217,15 +276,12 @@ def gauss_sum_fwd(q, k, v, tau, out=None, workspace=None, stream=None):
     N, C = v.shape
     p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
     lib = load()
-    if out is None:
-        out = torch.empty((M, C), dtype=torch.float32, device=q.device)
+    out = _output(out, "out", (M, C), q.device)
     need = int(lib.gauss_sum_fwd_workspace_size(ctypes.byref(p)))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, q.device)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, q.device)
     st = lib.gauss_sum_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), float(tau), _ptr(out),
                            _ptr(workspace), wbytes, _stream(stream))
+    _keep_alive(stream, out, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_fwd")
     return out
@@ -237,8 +293,7 @@ def gauss_sum_bwd(q, k, v, tau, dout, want=(True, True, True), workspace=None, s
     _check_inputs(q, k, v)
     M, D = q.shape
     N, C = v.shape
-    if not dout.is_cuda or dout.shape != (M, C) or not dout.is_contiguous():
-        raise ValueError("dout must be a contiguous %d x %d GPU tensor" % (M, C))
+    _check_tensor(dout, "dout", (M, C), q.device)
     p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
     lib = load()
     dev = q.device
@@ -247,13 +302,11 @@ def gauss_sum_bwd(q, k, v, tau, dout, want=(True, True, True), workspace=None, s
     dv = torch.empty((N, C), dtype=torch.float32, device=dev) if want[2] else None
     need = int(lib.gauss_sum_bwd_workspace_size(ctypes.byref(p), int(bool(want[0])),
                                                 int(bool(want[1])), int(bool(want[2]))))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, dev)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, dev)
     st = lib.gauss_sum_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), float(tau), _ptr(dout),
                            _dtype_code(dout.dtype), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace),
                            wbytes, _stream(stream))
+    _keep_alive(stream, dq, dk, dv, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_bwd")
     return dq, dk, dv
@@ -267,25 +320,21 @@ def gauss_sum_fwd_bwd(q, k, v, tau, dout, want=(True, True, True), out=None, wor
     _check_inputs(q, k, v)
     M, D = q.shape
     N, C = v.shape
-    if not dout.is_cuda or dout.shape != (M, C) or not dout.is_contiguous():
-        raise ValueError("dout must be a contiguous %d x %d GPU tensor" % (M, C))
+    _check_tensor(dout, "dout", (M, C), q.device)
     p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
     lib = load()
     dev = q.device
-    if out is None:
-        out = torch.empty((M, C), dtype=torch.float32, device=dev)
+    out = _output(out, "out", (M, C), dev)
     dq = torch.empty((M, D), dtype=torch.float32, device=dev) if want[0] else None
     dk = torch.empty((N, D), dtype=torch.float32, device=dev) if want[1] else None
     dv = torch.empty((N, C), dtype=torch.float32, device=dev) if want[2] else None
     need = int(lib.gauss_sum_fwd_bwd_workspace_size(ctypes.byref(p), int(bool(want[0])),
                                                     int(bool(want[1])), int(bool(want[2]))))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, dev)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, dev)
     st = lib.gauss_sum_fwd_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), float(tau), _ptr(dout),
                                _dtype_code(dout.dtype), _ptr(out), _ptr(dq), _ptr(dk), _ptr(dv),
                                _ptr(workspace), wbytes, _stream(stream))
+    _keep_alive(stream, out, dq, dk, dv, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_fwd_bwd")
     return out, dq, dk, dv
@@ -295,8 +344,8 @@ def _batched_inputs(q, k, v):
     """(B, M, N, D, C, strides) for q: B x M x D, k: B x N x D or N x D (shared),
     v: B x N x C or N x C (shared); contiguous GPU tensors."""
     for name, t in (("q", q), ("k", k), ("v", v)):
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError("%s must be a contiguous GPU tensor" % name)
+        if not t.is_contiguous():
+            raise ValueError("%s must be a contiguous tensor" % name)
     if q.dim() != 3:
         raise ValueError("q must be B x M x D")
     B, M, D = q.shape
@@ -307,6 +356,11 @@ def _batched_inputs(q, k, v):
         raise ValueError("inconsistent batch shapes")
     if q.dtype != k.dtype:
         raise TypeError("q and k must share a dtype")
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda:
+            raise ValueError("%s must be a GPU tensor" % name)
+    if k.device != q.device or v.device != q.device:
+        raise ValueError("q, k and v must be on one device")
     ks = N * D if k.dim() == 3 else 0
     vs = N * C if v.dim() == 3 else 0
     return B, M, N, D, C, M * D, ks, vs
@@ -332,16 +386,13 @@ def gauss_sum_fwd_batched(q, k, v, tau, out=None, workspace=None, stream=None, g
     B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
     p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
     lib = load()
-    if out is None:
-        out = torch.empty((B, M, C), dtype=torch.float32, device=q.device)
+    out = _output(out, "out", (B, M, C), q.device)
     b = Batch(B, qs, ks, vs, 0, M * C, 0, 0, 0)
     need = int(lib.gauss_sum_fwd_batched_workspace_size(ctypes.byref(p), int(group or max(B, 1))))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, q.device)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, q.device)
     st = lib.gauss_sum_fwd_batched(ctypes.byref(p), ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v),
                                    float(tau), _ptr(out), _ptr(workspace), wbytes, _stream(stream))
+    _keep_alive(stream, out, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_fwd_batched")
     return out
@@ -355,8 +406,7 @@ def gauss_sum_bwd_batched(q, k, v, tau, dout, want=(True, True, True), workspace
     (default: all B)."""
     import torch
     B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
-    if not dout.is_cuda or dout.shape != (B, M, C) or not dout.is_contiguous():
-        raise ValueError("dout must be a contiguous %d x %d x %d GPU tensor" % (B, M, C))
+    _check_tensor(dout, "dout", (B, M, C), q.device)
     if (want[1] and ks == 0) or (want[2] and vs == 0):
         raise ValueError("dk / dv of a shared key set: sum the per-problem gradients instead")
     p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
@@ -369,13 +419,11 @@ def gauss_sum_bwd_batched(q, k, v, tau, dout, want=(True, True, True), workspace
     need = int(lib.gauss_sum_bwd_batched_workspace_size(ctypes.byref(p), int(group or max(B, 1)),
                                                         int(bool(want[0])), int(bool(want[1])),
                                                         int(bool(want[2]))))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, dev)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, dev)
     st = lib.gauss_sum_bwd_batched(ctypes.byref(p), ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v),
                                    float(tau), _ptr(dout), _dtype_code(dout.dtype), _ptr(dq), _ptr(dk),
                                    _ptr(dv), _ptr(workspace), wbytes, _stream(stream))
+    _keep_alive(stream, dq, dk, dv, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_bwd_batched")
     return dq, dk, dv
@@ -396,15 +444,13 @@ def gauss_sum_fwd_bwd_batched(q, k, v, tau, dout, want=(True, True, True), out=N
     dq passes where gauss_sum_fwd_bwd fuses them."""
     import torch
     B, M, N, D, C, qs, ks, vs = _batched_inputs(q, k, v)
-    if not dout.is_cuda or dout.shape != (B, M, C) or not dout.is_contiguous():
-        raise ValueError("dout must be a contiguous %d x %d x %d GPU tensor" % (B, M, C))
+    _check_tensor(dout, "dout", (B, M, C), q.device)
     if (want[1] and ks == 0) or (want[2] and vs == 0):
         raise ValueError("dk / dv of a shared key set: sum the per-problem gradients instead")
     p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
     lib = load()
     dev = q.device
-    if out is None:
-        out = torch.empty((B, M, C), dtype=torch.float32, device=dev)
+    out = _output(out, "out", (B, M, C), dev)
     dq = torch.empty((B, M, D), dtype=torch.float32, device=dev) if want[0] else None
     dk = torch.empty((B, N, D), dtype=torch.float32, device=dev) if want[1] else None
     dv = torch.empty((B, N, C), dtype=torch.float32, device=dev) if want[2] else None
@@ -412,14 +458,12 @@ def gauss_sum_fwd_bwd_batched(q, k, v, tau, dout, want=(True, True, True), out=N
     need = int(lib.gauss_sum_fwd_bwd_batched_workspace_size(ctypes.byref(p), int(group or max(B, 1)),
                                                             int(bool(want[0])), int(bool(want[1])),
                                                             int(bool(want[2]))))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, dev)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, dev)
     st = lib.gauss_sum_fwd_bwd_batched(ctypes.byref(p), ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v),
                                        float(tau), _ptr(dout), _dtype_code(dout.dtype), _ptr(out),
                                        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), wbytes,
                                        _stream(stream))
+    _keep_alive(stream, out, dq, dk, dv, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_fwd_bwd_batched")
     return out, dq, dk, dv
@@ -437,7 +481,7 @@ def gauss_sum_mmd_flow(x, v, tau, want=(True, True, True), workspace=None, strea
     import torch
     _check_inputs(x, x, v)
     N, D = x.shape
-    if v.shape != (N, 1):
+    if tuple(v.shape) != (N, 1):
         raise ValueError("v must be N x 1")
     p = make_problem(N, N, D, 1, _dtype_code(x.dtype), _dtype_code(v.dtype))
     lib = load()
@@ -446,12 +490,10 @@ def gauss_sum_mmd_flow(x, v, tau, want=(True, True, True), workspace=None, strea
     grad = torch.empty((N, D), dtype=torch.float32, device=dev) if want[1] else None
     mmd2 = torch.empty((), dtype=torch.float64, device=dev) if want[2] else None
     need = int(lib.gauss_sum_mmd_flow_workspace_size(ctypes.byref(p)))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, dev)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, dev)
     st = lib.gauss_sum_mmd_flow(ctypes.byref(p), _ptr(x), _ptr(v), float(tau), _ptr(s), _ptr(grad),
                                 _ptr(mmd2), _ptr(workspace), wbytes, _stream(stream))
+    _keep_alive(stream, s, grad, mmd2, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_mmd_flow")
     return s, grad, mmd2
@@ -469,20 +511,17 @@ def gauss_sum_svgd(x, score, tau, out=None, workspace=None, stream=None):
     import torch
     _check_inputs(x, x, score)
     N, D = x.shape
-    if score.shape != (N, D):
+    if tuple(score.shape) != (N, D):
         raise ValueError("score must be N x D")
     p = make_problem(N, N, D, D, _dtype_code(x.dtype), _dtype_code(score.dtype))
     lib = load()
     dev = x.device
-    if out is None:
-        out = torch.empty((N, D), dtype=torch.float32, device=dev)
+    out = _output(out, "out", (N, D), dev)
     need = int(lib.gauss_sum_svgd_workspace_size(ctypes.byref(p)))
-    if workspace is None:
-        workspace, wbytes = _workspace(need, dev)
-    else:
-        wbytes = workspace.numel() * workspace.element_size()
+    workspace, wbytes = _workspace_arg(workspace, need, dev)
     st = lib.gauss_sum_svgd(ctypes.byref(p), _ptr(x), _ptr(score), float(tau), _ptr(out), _ptr(workspace),
                             wbytes, _stream(stream))
+    _keep_alive(stream, out, workspace)
     if st != 0:
         raise GaussSumError(st, "gauss_sum_svgd")
     return out

@@ -1,5 +1,5 @@
-"""ctypes binding of libgs_peaks.so: the device's own matrix-core, exp2, FMA
-and streaming-read rates, timed with HIP events on the caller's stream.
+"""ctypes binding of libgs_peaks.so: the device's own matrix-core, exp2, FMA,
+streaming-read and LDS-read rates, timed with HIP events on the caller's stream.
 
 `measure()` returns the rates as a dict; the work per launch follows the
 formulas stated in include/gs_peaks.h.  Raises if the library is missing or
@@ -13,7 +13,8 @@ LIB_PATH = os.path.join(os.path.dirname(HERE), "libgs_peaks.so")
 THREADS = 256
 MFMA_CHAINS = 4
 CHAINS = 8
-EXPORTED = ("gs_peaks_mfma", "gs_peaks_exp", "gs_peaks_fma", "gs_peaks_read")
+LDS_READS = 4
+EXPORTED = ("gs_peaks_mfma", "gs_peaks_exp", "gs_peaks_fma", "gs_peaks_read", "gs_peaks_lds")
 
 _lib = None
 
@@ -29,6 +30,7 @@ def load(path=LIB_PATH):
         lib.gs_peaks_exp.argtypes = [vp, i64, i32, vp]
         lib.gs_peaks_fma.argtypes = [vp, i64, i32, vp]
         lib.gs_peaks_read.argtypes = [vp, i64, vp, i64, vp]
+        lib.gs_peaks_lds.argtypes = [vp, i64, i32, vp]
         for name in EXPORTED:
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
@@ -63,7 +65,8 @@ def _time(torch, launch, reps, settle_s):
 
 def measure(read_bytes=4 << 30, reps=20, settle_s=0.3):
     """Measured rates on cuda:0: fp16 MFMA flop/s (both shapes), exp2/s,
-    fp32 FMA flop/s (unpacked) and streaming-read bytes/s."""
+    fp32 FMA flop/s (unpacked), streaming-read bytes/s and LDS-read bytes/s
+    (whole device)."""
     import torch
 
     lib = load()
@@ -85,6 +88,13 @@ def measure(read_bytes=4 << 30, reps=20, settle_s=0.3):
     res["exp2_per_s"] = wg * THREADS * iters * CHAINS / t
     t = _time(torch, lambda s: _check(lib.gs_peaks_fma(out.data_ptr(), wg, iters, s), "gs_peaks_fma"), reps, settle_s)
     res["fma_f32_flop_per_s"] = 2.0 * wg * THREADS * iters * CHAINS / t
+
+    # LDS reads: 8 workgroups per CU (at most 5 resident with 32 KiB each)
+    lds_wg, lds_iters = cus * 8, 512
+    rd = out.view(torch.int32)
+    t = _time(torch, lambda s: _check(lib.gs_peaks_lds(rd.data_ptr(), lds_wg, lds_iters, s), "gs_peaks_lds"),
+              reps, settle_s)
+    res["lds_read_bytes_per_s"] = lds_wg * THREADS * lds_iters * LDS_READS * 16 / t
 
     # streaming read: the best of three grid sizes (4, 8, 16 workgroups per CU)
     buf = torch.ones(read_bytes // 4, dtype=torch.int32, device=dev)

@@ -93,6 +93,30 @@ __global__ __launch_bounds__(kThreads) void k_read(const uint4* in, int64_t n, u
   out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = acc;
 }
 
+// LDS read bandwidth: every wave reads four independent 1-KiB rows per
+// iteration (lane l takes the 16 bytes at 16 l of each row, ds_read_b128 on
+// linear addresses), walking over the workgroup's kLdsBytes of LDS, folded
+// into one word per lane by xor.
+constexpr int kLdsBytes = 32768;
+__global__ __launch_bounds__(kThreads) void k_lds(uint32_t* out, int iters) {
+  __shared__ uint4 buf[kLdsBytes / 16];
+  for (int i = threadIdx.x; i < kLdsBytes / 16; i += kThreads)
+    buf[i] = uint4{(uint32_t)i, (uint32_t)(3 * i), (uint32_t)(5 * i), (uint32_t)(7 * i)};
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kRows = kLdsBytes / 1024;  // 1-KiB rows
+  uint32_t acc = 0;
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int u = 0; u < GS_PEAKS_LDS_READS; ++u) {
+      const int row = (i * GS_PEAKS_LDS_READS + u + 8 * wave) & (kRows - 1);
+      const uint4 a = buf[row * 64 + lane];
+      acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+  }
+  out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = acc;
+}
+
 bool bad_grid(int64_t workgroups) { return workgroups <= 0 || workgroups > 0x7fffffff; }
 
 int launched() { return hipGetLastError() == hipSuccess ? 0 : 2; }
@@ -132,5 +156,12 @@ extern "C" int gs_peaks_read(const void* in, int64_t bytes, uint32_t* out, int64
   (void)hipGetLastError();
   k_read<<<dim3((unsigned)workgroups), dim3(kThreads), 0, stream>>>(static_cast<const uint4*>(in),
                                                                     bytes / 16, out);
+  return launched();
+}
+
+extern "C" int gs_peaks_lds(uint32_t* out, int64_t workgroups, int32_t iters, hipStream_t stream) {
+  if (!out || bad_grid(workgroups) || iters <= 0) return 1;
+  (void)hipGetLastError();
+  k_lds<<<dim3((unsigned)workgroups), dim3(kThreads), 0, stream>>>(out, iters);
   return launched();
 }

@@ -173,13 +173,20 @@ def make(name: str, seed: int = 0, M: Optional[int] = None, N: Optional[int] = N
 
     if name == "rect_d256":
         def unit(n):
-            # N(0, I) rows divided by their norm (computed in fp64), stored fp16
-            x = rng.standard_normal((n, D), dtype=f32)
+            # N(0, I) rows divided by their norm (computed in fp64), stored
+            # fp16; drawn in blocks of rows into reused buffers (the same
+            # stream of draws as one call for all n rows)
+            blk_rows = 4096
             h = np.empty((n, D), dtype=np.float16)
-            for a in range(0, n, 1 << 16):
-                blk = x[a:a + (1 << 16)].astype(np.float64)
+            x = np.empty((blk_rows, D), dtype=f32)
+            buf = np.empty((blk_rows, D), dtype=np.float64)
+            for a in range(0, n, blk_rows):
+                m = min(blk_rows, n - a)
+                rng.standard_normal(out=x[:m], dtype=f32)
+                blk = buf[:m]
+                blk[...] = x[:m]
                 blk /= np.sqrt(np.einsum("ij,ij->i", blk, blk))[:, None]
-                h[a:a + (1 << 16)] = blk.astype(np.float16)
+                h[a:a + m] = blk
             return h
         q = qv = unit(M)
         k = kv = unit(N)

@@ -76,3 +76,35 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr + r.stdout
+
+
+def test_algorithmic_step_flops():
+    # forward alone, forward + dq on shared tiles, forward + full backward
+    assert bench.algorithmic_flops_per_pair(("fwd",), 16, 1) == 2 * 16 + 2
+    assert bench.algorithmic_flops_per_pair(("fwd", "dq"), 64, 1) == 4 * 64 + 4
+    assert bench.algorithmic_flops_per_pair(("fwd", "dq", "dk", "dv"), 256, 16) == 8 * 256 + 6 * 16
+    assert bench.algorithmic_flops_per_pair(("dq",), 64, 8) == 4 * 64 + 2 * 8
+    assert bench.algorithmic_flops_per_pair(("dv",), 64, 8) == 2 * 64 + 2 * 8
+
+
+def test_dominant_launch_flops_follow_the_fusion_rule():
+    # D = 256, C = 16: nothing fused; dq and dk launches 4D+2C each
+    assert bench.dominant_flops(("fwd", "dq", "dk", "dv"), 256, 16, True) == 4 * 256 + 2 * 16
+    # single channel: forward fused into dq, dv into dk
+    assert bench.dominant_flops(("fwd", "dq"), 64, 1, True) == 4 * 64 + 4
+    assert bench.dominant_flops(("fwd", "dq"), 64, 1, False) == 4 * 64 + 2
+    assert bench.dominant_flops(("fwd",), 32, 4, False) == 2 * 32 + 2 * 4
+
+
+def test_sub_record_fields(monkeypatch):
+    monkeypatch.setattr(bench, "measured_peaks", lambda: {"exp2_per_s": 1.0e13})
+    res = {"config": {"workload": "mixture_d32: ...", "M": 1024, "N": 2048, "D": 32, "C": 4, "tau": 1.0,
+                      "passes": "fwd", "api": "gauss_sum_fwd"},
+           "steps": 5, "ms_per_step": 2.0, "value": 1024 * 2048 / 2e-3,
+           "step_roofline": {"frac": 0.1},
+           "roofline": {"kernel": "k_fwd", "avg_launch_ms": 1.0, "frac": 0.2, "exp": {"achieved": 1024 * 2048 / 1e-3}}}
+    r = bench.sub_record(res)
+    assert r["workload"] == "mixture_d32"
+    assert r["exp_per_s_step"] == pytest.approx(1024 * 2048 / 2e-3)
+    assert r["step_frac_of_measured_exp_rate"] == pytest.approx(1024 * 2048 / 2e-3 / 1e13)
+    assert r["kernel_frac_of_measured_exp_rate"] == pytest.approx(1024 * 2048 / 1e-3 / 1e13)

@@ -32,4 +32,6 @@ def test_measured_rates_are_plausible():
     for key, nominal in (("mfma_f16_16x16x32_flop_per_s", 2.5e15), ("mfma_f16_32x32x16_flop_per_s", 2.5e15),
                          ("exp2_per_s", 256 * 4 * 8 * 2.4e9), ("fma_f32_flop_per_s", 157.3e12)):
         assert 0.05 * nominal < r[key] < 1.05 * nominal, (key, r[key])
+    # LDS: between 128 and 256 bytes per CU and clock at 2.4 GHz
+    assert 0.05 * 256 * 128 * 2.4e9 < r["lds_read_bytes_per_s"] < 1.05 * 256 * 256 * 2.4e9
     assert 1e11 < r["read_bytes_per_s"] < 2e13   # a 256 MiB buffer may be served from the 256 MB cache

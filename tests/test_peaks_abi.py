@@ -22,7 +22,7 @@ def test_exports_every_declared_symbol():
     assert names <= exported
     # the header's constants are the binding's
     for macro, val in (("GS_PEAKS_THREADS", peaks.THREADS), ("GS_PEAKS_MFMA_CHAINS", peaks.MFMA_CHAINS),
-                       ("GS_PEAKS_CHAINS", peaks.CHAINS)):
+                       ("GS_PEAKS_CHAINS", peaks.CHAINS), ("GS_PEAKS_LDS_READS", peaks.LDS_READS)):
         assert re.search(r"#define %s (\d+)" % macro, text).group(1) == str(val)
 
 
@@ -41,3 +41,6 @@ def test_invalid_arguments_rejected_before_launch():
     assert lib.gs_peaks_read(FAKE + 8, 16, FAKE, 4, None) == 1    # misaligned
     assert lib.gs_peaks_read(FAKE, 0, FAKE, 4, None) == 1
     assert lib.gs_peaks_read(FAKE, 16, None, 4, None) == 1
+    assert lib.gs_peaks_lds(None, 4, 1, None) == 1
+    assert lib.gs_peaks_lds(FAKE, 0, 1, None) == 1
+    assert lib.gs_peaks_lds(FAKE, 4, 0, None) == 1
