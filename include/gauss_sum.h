@@ -72,7 +72,9 @@ typedef enum {
   GS_ERR_WORKSPACE = 6,    /* workspace NULL or smaller than required */
   GS_ERR_HIP = 7,          /* a HIP runtime call or kernel launch failed */
   GS_ERR_INTERNAL = 8,     /* unexpected internal failure */
-  GS_ERR_ALIAS = 9         /* an output overlaps an input or another output */
+  GS_ERR_ALIAS = 9,        /* an output overlaps an input or another output */
+  GS_ERR_SCRATCH_LIMIT = 10 /* gauss_sum_fwd_noalloc: the problem needs more scratch than
+                               GAUSS_SUM_NOALLOC_SCRATCH_BYTES */
 } gs_status;
 
 /* Problem description.  qk_dtype: GS_F16 or GS_BF16 (both q and k), or
@@ -101,6 +103,26 @@ size_t gauss_sum_bwd_workspace_size(const gs_problem* p, int want_dq, int want_d
  * M == 0 is a no-op; N == 0 writes zeros. */
 gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
                         float* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Largest workspace gauss_sum_fwd_noalloc can serve from its built-in
+ * scratch array (128 MiB per GPU). */
+#define GAUSS_SUM_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/* gauss_sum_fwd without a workspace argument and without any allocation,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments, validation and results as gauss_sum_fwd (bitwise: the same
+ * kernels and launch plan); the workspace is a file-scope device array of
+ * the library, GAUSS_SUM_NOALLOC_SCRATCH_BYTES bytes on every GPU the call
+ * is made on, held until the process ends.  Returns GS_ERR_SCRATCH_LIMIT
+ * (nothing launched) when gauss_sum_fwd_workspace_size(p) exceeds that size.
+ * Every call on one GPU uses the same array: calls that may overlap in time
+ * on one GPU (different streams without ordering, other host threads) race
+ * and give undefined results; order them on one stream.  The first call on
+ * a GPU looks up the array's device address (no allocation); every call
+ * overwrites what it uses of the array before reading it. */
+gs_status gauss_sum_fwd_noalloc(const gs_problem* p, const void* q, const void* k, const void* v,
+                                float tau, float* out, hipStream_t stream);
 
 /* Backward: for L = sum_{m,c} dout[m,c] s[m,c] (dout: M x C of dout_dtype,
  * GS_F32, GS_F16 or GS_BF16) writes

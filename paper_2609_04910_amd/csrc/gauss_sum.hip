@@ -906,6 +906,7 @@ const char* gauss_sum_status_string(gs_status s) {
     case GS_ERR_HIP: return "HIP runtime error";
     case GS_ERR_INTERNAL: return "internal error";
     case GS_ERR_ALIAS: return "an output overlaps an input or another output";
+    case GS_ERR_SCRATCH_LIMIT: return "problem needs more scratch than the no-allocation entry point holds";
   }
   return "unknown status";
 }
@@ -945,7 +946,36 @@ int gauss_sum_profile_stop(float* ms, int max) {
 }  // extern "C"
 
 namespace gs {
+
+// Workspace of gauss_sum_fwd_noalloc: a file-scope device array (one copy
+// per GPU, held until the process ends).  Host code never uses the symbol
+// itself as an address: its device address on the current GPU comes from
+// hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = GAUSS_SUM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// Device address of `scratch` on the current GPU (looked up on the first
+// call per device, with that device current).
+gs_status scratch_address(void** ptr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return GS_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return GS_ERR_UNSUPPORTED;
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = p;
+  });
+  if (g_scratch_err[dev] != hipSuccess || !g_scratch_ptr[dev]) return GS_ERR_HIP;
+  *ptr = g_scratch_ptr[dev];
+  return GS_SUCCESS;
+}
 
 // Problems per launch group at most (grid.z).
 constexpr int64_t kMaxGroup = 65535;
@@ -1152,6 +1182,18 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
 extern "C" {
 
 size_t gauss_sum_fwd_workspace_size(const gs_problem* p) { return workspace_for(p, true, 0, 0, 0); }
+
+gs_status gauss_sum_fwd_noalloc(const gs_problem* p, const void* q, const void* k, const void* v,
+                                float tau, float* out, hipStream_t stream) {
+  gs_status st = check_problem(p);
+  if (st != GS_SUCCESS || (st = check_tau(tau)) != GS_SUCCESS) return st;
+  const size_t need = workspace_for(p, true, 0, 0, 0);
+  if (need > kScratchBytes) return GS_ERR_SCRATCH_LIMIT;
+  void* ws = nullptr;
+  if (need > 0 && (st = scratch_address(&ws)) != GS_SUCCESS) return st;
+  return run(p, nullptr, q, k, v, tau, nullptr, GS_F32, out, nullptr, nullptr, nullptr, ws,
+             need > 0 ? kScratchBytes : 0, stream);
+}
 
 size_t gauss_sum_bwd_workspace_size(const gs_problem* p, int want_dq, int want_dk, int want_dv) {
   if (!want_dq && !want_dk && !want_dv) return 0;

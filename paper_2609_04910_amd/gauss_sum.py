@@ -29,15 +29,17 @@ GS_F32, GS_F16, GS_BF16 = 0, 1, 2
 STATUS = {
     0: "GS_SUCCESS", 1: "GS_ERR_NULL_POINTER", 2: "GS_ERR_BAD_SHAPE", 3: "GS_ERR_BAD_TAU",
     4: "GS_ERR_UNSUPPORTED", 5: "GS_ERR_MISALIGNED", 6: "GS_ERR_WORKSPACE", 7: "GS_ERR_HIP",
-    8: "GS_ERR_INTERNAL", 9: "GS_ERR_ALIAS",
+    8: "GS_ERR_INTERNAL", 9: "GS_ERR_ALIAS", 10: "GS_ERR_SCRATCH_LIMIT",
 }
+NOALLOC_SCRATCH_BYTES = 128 << 20   # GAUSS_SUM_NOALLOC_SCRATCH_BYTES
 EXPORTED = ("gauss_sum_fwd", "gauss_sum_bwd", "gauss_sum_fwd_bwd", "gauss_sum_fwd_workspace_size",
             "gauss_sum_bwd_workspace_size", "gauss_sum_fwd_bwd_workspace_size",
             "gauss_sum_status_string", "gauss_sum_abi_version", "gauss_sum_profile_start",
             "gauss_sum_profile_stop", "gauss_sum_mmd_flow", "gauss_sum_mmd_flow_workspace_size",
             "gauss_sum_fwd_batched", "gauss_sum_bwd_batched", "gauss_sum_fwd_batched_workspace_size",
             "gauss_sum_bwd_batched_workspace_size", "gauss_sum_fwd_bwd_batched",
-            "gauss_sum_fwd_bwd_batched_workspace_size", "gauss_sum_svgd", "gauss_sum_svgd_workspace_size")
+            "gauss_sum_fwd_bwd_batched_workspace_size", "gauss_sum_svgd", "gauss_sum_svgd_workspace_size",
+            "gauss_sum_fwd_noalloc")
 PROFILE_FWD, PROFILE_GRAD = 1, 2
 
 
@@ -79,6 +81,8 @@ def load(path=LIB_PATH):
     lib.gauss_sum_bwd_workspace_size.restype = sz
     lib.gauss_sum_fwd.argtypes = [P, vp, vp, vp, ctypes.c_float, f32p, vp, sz, vp]
     lib.gauss_sum_fwd.restype = ctypes.c_int
+    lib.gauss_sum_fwd_noalloc.argtypes = [P, vp, vp, vp, ctypes.c_float, f32p, vp]
+    lib.gauss_sum_fwd_noalloc.restype = ctypes.c_int
     lib.gauss_sum_bwd.argtypes = [P, vp, vp, vp, ctypes.c_float, vp, ctypes.c_int, f32p, f32p, f32p,
                                   vp, sz, vp]
     lib.gauss_sum_bwd.restype = ctypes.c_int
@@ -285,6 +289,28 @@ def gauss_sum_fwd(q, k, v, tau, out=None, workspace=None, stream=None):
     if st != 0:
         raise GaussSumError(st, "gauss_sum_fwd")
     return out
+
+
+def gauss_sum_fwd_noalloc(q, k, v, tau, out, stream=None):
+    """gauss_sum_fwd through the entry point that allocates nothing (its
+    workspace is the library's built-in scratch array on the current GPU);
+    `out` (M x C fp32) is required.  Calls that overlap in time on one GPU
+    race; order them on one stream."""
+    _check_inputs(q, k, v)
+    M, D = q.shape
+    N, C = v.shape
+    _check_tensor(out, "out", (M, C), q.device, _torch().float32)
+    p = make_problem(M, N, D, C, _dtype_code(q.dtype), _dtype_code(v.dtype))
+    st = load().gauss_sum_fwd_noalloc(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), float(tau), _ptr(out),
+                                      _stream(stream))
+    if st != 0:
+        raise GaussSumError(st, "gauss_sum_fwd_noalloc")
+    return out
+
+
+def _torch():
+    import torch
+    return torch
 
 
 def gauss_sum_bwd(q, k, v, tau, dout, want=(True, True, True), workspace=None, stream=None):

@@ -36,11 +36,11 @@ def test_library_loads_and_exports_every_declared_symbol():
 def test_abi_version_and_status_strings():
     assert gs.gauss_sum_abi_version() == 1
     seen = set()
-    for code in range(10):
+    for code in range(11):
         s = gs.status_string(code)
         assert s and s != "unknown status"
         seen.add(s)
-    assert len(seen) == 10
+    assert len(seen) == 11
     assert gs.status_string(1234) == "unknown status"
 
 
@@ -296,6 +296,29 @@ def test_profile_hook_arguments():
     assert lib.gauss_sum_profile_stop(None, 0) == 0  # nothing started
 
 
+def _noalloc(M=8, N=8, D=4, C=2, tau=1.0, p=True, out=FAKE + 0x30000):
+    lib = gs.load()
+    prob = gs.make_problem(M, N, D, C, gs.GS_F16, gs.GS_F32)
+    return lib.gauss_sum_fwd_noalloc(ctypes.byref(prob) if p else None, FAKE, FAKE + 0x10000,
+                                     FAKE + 0x20000, ctypes.c_float(tau), out, None)
+
+
+def test_noalloc_validation_and_scratch_limit():
+    assert _noalloc(p=False) == 1
+    assert _noalloc(D=0) == 2
+    assert _noalloc(tau=0.0) == 3
+    # the built-in scratch holds GAUSS_SUM_NOALLOC_SCRATCH_BYTES: larger
+    # problems are refused before anything is looked up or launched
+    for M, N, D, C in ((1 << 22, 1 << 22, 256, 16), (1 << 20, 1 << 20, 64, 1), (4096, 1 << 22, 128, 1)):
+        need = gs.gauss_sum_fwd_workspace_size(M, N, D, C)
+        assert need > gs.NOALLOC_SCRATCH_BYTES
+        assert _noalloc(M, N, D, C) == 10
+    assert gs.gauss_sum_fwd_workspace_size(8, 8, 4, 2) <= gs.NOALLOC_SCRATCH_BYTES
+    hdr = open(os.path.join(ROOT, "include", "gauss_sum.h")).read()
+    assert "#define GAUSS_SUM_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)" in hdr
+    assert gs.NOALLOC_SCRATCH_BYTES == 128 << 20
+
+
 def test_no_device_reports_hip_error():
     # A valid call in a process without a usable GPU fails at launch, and the
     # failure is reported as GS_ERR_HIP rather than crashing.
@@ -303,6 +326,7 @@ def test_no_device_reports_hip_error():
     if torch.cuda.is_available():
         pytest.skip("a GPU is visible")
     assert _fwd() == 7
+    assert _noalloc() == 7
     assert _bwd() == 7
     assert _fb() == 7
     assert _flow() == 7
