@@ -75,9 +75,33 @@ constexpr int fwd_qt(int DP, int CT) {
 // Every workgroup's rows lie inside the padded row range.
 static_assert(kRowPad % (kBlockThreads / 4 * 8) == 0 && kRowPad % 256 == 0, "row padding vs. query tiles");
 
+
+// Waves per workgroup of the gradient and forward kernels: eight for D > 64,
+// where a key step's operands take 12 to 34 KiB of LDS -- one workgroup per
+// CU then holds a deeper ring (three or four stages) that feeds twice the
+// queries of a four-wave workgroup, half the copies per pair (D = 256,
+// C = 16: dq pass 378 -> 265 ms, forward 124 -> 107 ms; D = C = 128: 5 %);
+// four for D <= 64 (no gain there).
+constexpr int dq_wpb(int DP) { return DP >= 4 ? 2 * kWavesPerBlock : kWavesPerBlock; }
+constexpr int fwd_wpb(int DP) { return DP >= 4 ? 2 * kWavesPerBlock : kWavesPerBlock; }
+
 constexpr int dq_qt(int DP, int CW) {
   return DP >= 4 ? (DP == 8 && CW == 8 ? 1 : 2) : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
 }
+
+// Every workgroup of a main kernel covers at most kRowPad query rows (the
+// padded row count of every operand copy is a multiple of kRowPad).
+constexpr bool tiles_within_padding() {
+  const int dps[4] = {1, 2, 4, 8}, cts[6] = {0, 1, 2, 4, 8, 16}, cws[5] = {0, 1, 2, 4, 8};
+  for (int dp : dps) {
+    for (int ct : cts)
+      if (16 * fwd_qt(dp, ct) * fwd_wpb(dp) > kRowPad) return false;
+    for (int cw : cws)
+      if (16 * dq_qt(dp, cw) * dq_wpb(dp) > kRowPad) return false;
+  }
+  return true;
+}
+static_assert(tiles_within_padding(), "query rows of a workgroup exceed the row padding");
 
 // ------------------------------------------------------------ dispatch tables
 
@@ -92,10 +116,10 @@ void launch_fwd(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, co
                 const uint32_t* vslot, float tau2, int64_t M, int C, int steps, int sps, float* out,
                 int64_t pstride, const Bz& bz) {
   if (grid.z > 1)
-    hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, true>), grid, dim3(kBlockThreads), 0, st,
+    hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, true, fwd_wpb(DP)>), grid, dim3(kWave * fwd_wpb(DP)), 0, st,
                        qs, nhq, srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride, bz);
   else
-    hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, false>), grid, dim3(kBlockThreads), 0, st,
+    hipLaunchKernelGGL((k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, false, fwd_wpb(DP)>), grid, dim3(kWave * fwd_wpb(DP)), 0, st,
                        qs, nhq, srt, snh, ks, scal, vt, vslot, tau2, M, C, steps, sps, out, pstride, bz);
 }
 
@@ -108,7 +132,7 @@ struct FwdK {
 template <typename T, int DP, int CT, bool ONE>
 FwdK fwd_k() {
   return {&launch_fwd<T, DP, CT, ONE>,
-          reinterpret_cast<const void*>(&k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, false>)};
+          reinterpret_cast<const void*>(&k_fwd<T, DP, CT, fwd_qt(DP, CT), ONE, false, fwd_wpb(DP)>)};
 }
 
 // CT = 0 selects the single-channel form (one 16-row tile of signs).
@@ -150,11 +174,11 @@ void launch_dq(dim3 grid, hipStream_t st, const uint4* qs, const float* nhq, con
                int D, int steps, int sps, float* out, int64_t pstride, const uint4* vt, int C,
                float* out_s, int64_t pstride_s, const Bz& bz) {
   if (grid.z > 1)
-    hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT, true>), grid, dim3(kBlockThreads), 0, st, qs,
+    hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT, true, dq_wpb(DP)>), grid, dim3(kWave * dq_wpb(DP)), 0, st, qs,
                        nhq, srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, g1, g1_dtype, tau2, tau,
                        M, D, steps, sps, out, pstride, vt, C, out_s, pstride_s, bz);
   else
-    hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT, false>), grid, dim3(kBlockThreads), 0, st, qs,
+    hipLaunchKernelGGL((k_dq<T, DP, CW, dq_qt(DP, CW), FCT, false, dq_wpb(DP)>), grid, dim3(kWave * dq_wpb(DP)), 0, st, qs,
                        nhq, srt, snh, ks, scal, kt, kslot, vs, vslot, gsr, gslot, g1, g1_dtype, tau2, tau,
                        M, D, steps, sps, out, pstride, vt, C, out_s, pstride_s, bz);
 }
@@ -167,7 +191,7 @@ struct DqK {
 template <typename T, int DP, int CW, int FCT>
 DqK dq_k() {
   return {&launch_dq<T, DP, CW, FCT>,
-          reinterpret_cast<const void*>(&k_dq<T, DP, CW, dq_qt(DP, CW), FCT, false>)};
+          reinterpret_cast<const void*>(&k_dq<T, DP, CW, dq_qt(DP, CW), FCT, false, dq_wpb(DP)>)};
 }
 
 // fused: also produce the forward sum (one 16-row tile: C = 1 through the
@@ -320,7 +344,7 @@ struct PassShape {
 // Workgroups of `kernel` resident on the current device at once (CUs times
 // workgroups per CU), cached per kernel and device; kDefaultSlots when no
 // device can be queried (workspace sizes asked for on a machine without one).
-int device_slots(const void* kernel) {
+int device_slots(const void* kernel, int threads) {
   struct Entry {
     const void* kernel;
     int device, slots;
@@ -336,7 +360,7 @@ int device_slots(const void* kernel) {
   int cus = 0, occ = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
     return kDefaultSlots;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, kBlockThreads, 0) != hipSuccess ||
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, 0) != hipSuccess ||
       occ < 1)
     return kDefaultSlots;
   const int slots = cus * occ;
@@ -349,11 +373,12 @@ int device_slots(const void* kernel) {
 // (rounds of resident workgroups) x (steps per split + fixed cost), searched
 // from the smallest count that fills the device once up to four times that.
 // `group` problems run side by side on grid.z.
-PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel, int64_t group) {
+PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel, int64_t group,
+                     int wpb = kWavesPerBlock) {
   PassShape ps;
-  ps.blocks = (int)ceil_div(rows, 64 * QT);
+  ps.blocks = (int)ceil_div(rows, 16 * QT * wpb);
   ps.steps = (int)ceil_div(keys, kStep);
-  const int64_t slots = device_slots(kernel);
+  const int64_t slots = device_slots(kernel, kWave * wpb);
   const int64_t wide = (int64_t)std::max(1, ps.blocks) * std::max<int64_t>(1, group);
   const int cap = std::max(1, ps.steps / kMinStepsPerSplit);
   const int need = (int)std::max<int64_t>(1, ceil_div(ps.steps, kMaxStepsPerSplit));
@@ -487,23 +512,24 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
 
   // Partial-sum buffer for split passes (reused by every pass in turn).
   size_t part = 0, part_s = 0;
-  auto consider = [&](int64_t rows, int64_t keys, int QT, int64_t width, const void* kernel) {
-    PassShape ps = pass_shape(rows, keys, QT, kernel, G);
+  auto consider = [&](int64_t rows, int64_t keys, int QT, int64_t width, const void* kernel,
+                      int wpb = kWavesPerBlock) {
+    PassShape ps = pass_shape(rows, keys, QT, kernel, G, wpb);
     if (ps.splits > 1) part = std::max(part, (size_t)ps.splits * rows * width * 4);
     return ps.splits;
   };
   const int qf = fwd_qt(pl.dm.DP, pl.dm.CT), qd = dq_qt(pl.dm.DP, dq_cw(p, pl.dm));
   const void* kf = fwd_kernel(p, pl.dm);
-  if (w.fwd && !w.fused()) consider(p.M, p.N, qf, p.C, kf);
+  if (w.fwd && !w.fused()) consider(p.M, p.N, qf, p.C, kf, fwd_wpb(pl.dm.DP));
   if (w.dq) {
-    const int sp = consider(p.M, p.N, qd, p.D, dq_kernel(p, pl.dm, w.fused()));
+    const int sp = consider(p.M, p.N, qd, p.D, dq_kernel(p, pl.dm, w.fused()), dq_wpb(pl.dm.DP));
     if (w.fused() && sp > 1) part_s = (size_t)sp * p.M * p.C * 4;
   }
   if (w.dk) {
-    const int sp = consider(p.N, p.M, qd, p.D, dq_kernel(p, pl.dm, w.fused_kv()));
+    const int sp = consider(p.N, p.M, qd, p.D, dq_kernel(p, pl.dm, w.fused_kv()), dq_wpb(pl.dm.DP));
     if (w.fused_kv() && sp > 1) part_s = std::max(part_s, (size_t)sp * p.N * p.C * 4);
   }
-  if (w.dv && !w.fused_kv()) consider(p.N, p.M, qf, p.C, kf);
+  if (w.dv && !w.fused_kv()) consider(p.N, p.M, qf, p.C, kf, fwd_wpb(pl.dm.DP));
   pl.part = part ? cv.take<float>(part) : nullptr;
   pl.part_s = part_s ? cv.take<float>(part_s) : nullptr;
   pl.total = cv.off;
@@ -691,7 +717,7 @@ void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t 
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
   const FwdK fk = fwd_for(p, dm);
-  PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT), fk.kernel, c.pl->G);
+  PassShape ps = pass_shape(nq, nk, fwd_qt(dm.DP, dm.CT), fk.kernel, c.pl->G, fwd_wpb(dm.DP));
   const bool split = ps.splits > 1;
   float* dst = split ? c.pl->part : out;
   Bz bz = bz_ws(c);
@@ -718,7 +744,7 @@ void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t n
   const Dims& dm = c.pl->dm;
   const bool fused = out_s != nullptr;
   const DqK dk = dq_for(p, dm, fused);
-  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, dq_cw(p, dm)), dk.kernel, c.pl->G);
+  PassShape ps = pass_shape(nq, nk, dq_qt(dm.DP, dq_cw(p, dm)), dk.kernel, c.pl->G, dq_wpb(dm.DP));
   const bool split = ps.splits > 1;
   float* dst = split ? c.pl->part : out;
   float* dst_s = fused ? (split ? c.pl->part_s : out_s) : nullptr;

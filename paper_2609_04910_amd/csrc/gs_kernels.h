@@ -6,11 +6,12 @@
 //          P = Phi * w.  The same kernel gives dk with the roles of (q, g) and
 //          (k, v) exchanged, and k_fwd gives dv = sum_m Phi g_m likewise.
 //
-// Work decomposition: a workgroup is 4 waves that share one stream of key
-// steps (32 keys each) through a three-stage LDS ring; wave w owns 16*QT
-// queries whose operands stay in registers.  Step s+2 is copied HBM -> LDS
-// with the gfx950 direct loads (global_load_lds_dwordx4, no register round
-// trip) while step s is computed, one barrier per step.  Per step and query tile a wave computes two
+// Work decomposition: a workgroup is 4 waves (8 for D > 64: one workgroup
+// per CU, the same ring then feeds twice the queries) that share one stream
+// of key steps (32 keys each) through a two- to four-stage LDS ring; wave w
+// owns 16*QT queries whose operands stay in registers.  Later steps are
+// copied HBM -> LDS with the gfx950 direct loads (buffer_load ... lds, no
+// register round trip) while step s is computed, one barrier per step.  Per step and query tile a wave computes two
 // 16x16 tiles of S~^T[n][m] = q_m.k_n - ||k_n||^2/2 on the matrix cores (the
 // key half-norm enters as the accumulator input, so it costs no vector
 // instruction), forms the exponent x = tau' S~ + (-tau'||q_m||^2/2 - off_m)
@@ -103,19 +104,28 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return (uint32_t)(uintptr_t)(const lds_void*)p;
 }
 
-// LDS ring of NS (3 or 2) stages over the key steps [s_begin, s_end): step
+// LDS ring of NS (2 to 4) stages over the key steps [s_begin, s_end): step
 // s+NS-1 streams in while step s is computed, with one barrier per step.
-// issue(s, k) enqueues the NL loads of step s into stage k; compute(k)
-// consumes stage k.  With three stages the wait for step s leaves the NL
-// loads of step s+1 in flight.
+// issue(s, k) enqueues the NL loads of step s into stage k (waves that copy
+// nothing see their wait satisfied at once and rely on the barrier, which
+// follows the copying waves' waits); compute(k) consumes stage k.  With
+// three stages the wait for step s leaves the NL loads of step s+1 in
+// flight, with four those of steps s+1 and s+2.
 template <int NS, int NL, typename Issue, typename Compute>
 __device__ __forceinline__ void key_stream(int s_begin, int s_end, Issue issue, Compute compute) {
-  static_assert(NS == 2 || NS == 3, "two or three stages");
+  static_assert(NS >= 2 && NS <= 4, "two to four stages");
   for (int k = 0; k < NS - 1; ++k)
     if (s_begin + k < s_end) issue(s_begin + k, k);
   int cur = 0;
   for (int s = s_begin; s < s_end; ++s) {
-    if constexpr (NS == 3) {
+    if constexpr (NS == 4) {
+      if (s + 2 < s_end)
+        wait_vmcnt<2 * NL>();  // steps s+1 and s+2 may still be in flight
+      else if (s + 1 < s_end)
+        wait_vmcnt<NL>();
+      else
+        wait_vmcnt<0>();
+    } else if constexpr (NS == 3) {
       if (s + 1 < s_end)
         wait_vmcnt<NL>();  // only step s+1 may still be in flight
       else
@@ -133,6 +143,16 @@ __device__ __forceinline__ void key_stream(int s_begin, int s_end, Issue issue, 
     compute(cur);
     cur = cur == NS - 1 ? 0 : cur + 1;
   }
+}
+
+// Stages for an eight-wave workgroup (one per CU) and a step of
+// `stage_bytes` with `loads` copies per copying wave: four if they fit in
+// 160 KiB of LDS and the vmcnt field (two steps in flight), else three,
+// else two.
+constexpr int wide_stages(int stage_bytes, int loads) {
+  if (4 * stage_bytes <= 160 * 1024 && 2 * loads < 64) return 4;
+  if (3 * stage_bytes <= 160 * 1024 && loads < 64) return 3;
+  return 2;
 }
 
 // Stages for a step of `stage_bytes`: three when two workgroups per CU still
@@ -378,8 +398,8 @@ __device__ __forceinline__ void store_row4(float* row, int c0, int width, bool v
 //
 // BZ: a batch of problems on grid.z (operands at the strides of bz); the
 // instance for one problem never reads bz.
-template <typename T, int DP, int CT, int QT, bool ONE, bool BZ>
-__global__ __launch_bounds__(kBlockThreads) void k_fwd(
+template <typename T, int DP, int CT, int QT, bool ONE, bool BZ, int WPB>
+__global__ __launch_bounds__(kWave * WPB) void k_fwd(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
     const uint4* __restrict__ vt, const uint32_t* __restrict__ vslot, float tau2, int64_t M, int C,
@@ -398,14 +418,18 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
   constexpr int KCH = 2 * DP;   // 1-KiB chunks of keys per step
   constexpr int NCH = KCH + CT; // + chunks of V^T
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
-  constexpr int NS = ring_stages(STAGE, NCH + 1);
+  // eight waves (one workgroup per CU, up to four stages): waves 0-3 copy
+  // every chunk, waves 4-7 none (splitting the copies between the two groups
+  // measured slower)
+  constexpr bool WIDE = WPB == 2 * kWavesPerBlock;
+  constexpr int NS = WIDE ? wide_stages(STAGE, NCH + 1) : ring_stages(STAGE, NCH + 1);
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t dlane = dma_lane_offset(lane);
   const int wave = threadIdx.x / kWave;
   const int j = lane & 15, g = lane >> 4;
-  const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * (16 * QT);
+  const int64_t q0 = ((int64_t)blockIdx.x * WPB + wave) * (16 * QT);
   const int s_begin = blockIdx.y * steps_per_split;
   const int s_end = min(steps_total, s_begin + steps_per_split);
   out += blockIdx.y * part_stride;
@@ -467,7 +491,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
       for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, dlane);
       dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
     };
-    key_stream<NS, KCH + 1>(s_begin, s_end, issue_k, [&](int stage) {
+    auto exact_compute = [&](int stage) {
       if (level != 2) return;
       const char* base = lds + stage * STAGE;
       const uint4* kb = reinterpret_cast<const uint4*>(base);
@@ -480,7 +504,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) smax[qt] = max_into(smax[qt], score_tile<T, DP>(kr, qreg[qt], cin));
       }
-    });
+    };
+    key_stream<NS, KCH + 1>(s_begin, s_end, issue_k, exact_compute);
     __syncthreads();  // every wave is done with the ring before the main stream refills it
     if (level == 2) {
 #pragma unroll
@@ -604,8 +629,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_fwd(
 // per CU: the large-D / large-C instances would otherwise take a few more
 // registers and run one wave per SIMD, which costs far more than the spill
 // of a few values outside the key loop.
-template <typename T, int DP, int CW, int QT, int FCT, bool BZ>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_dq(
+template <typename T, int DP, int CW, int QT, int FCT, bool BZ, int WPB>
+__global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))) void k_dq(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
     const uint4* __restrict__ kt_ks, const uint32_t* __restrict__ kslot, const uint4* __restrict__ vs,
@@ -639,7 +664,10 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
   constexpr int FCH = CW > 0 ? FCT : 0;     // chunks of V^T (KS) per step, fused forward
   constexpr int NCH = KCH + VCH + TCH + FCH;
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
-  constexpr int NS = ring_stages(STAGE, NCH + 1);
+  // eight waves (one workgroup per CU): waves 0-3 copy every chunk, waves 4-7
+  // none (splitting the copies between the two groups measured slower here)
+  constexpr bool WIDE = WPB == 2 * kWavesPerBlock;
+  constexpr int NS = WIDE ? wide_stages(STAGE, NCH + 1) : ring_stages(STAGE, NCH + 1);
   constexpr int GW = CW > 0 ? CW : 1;       // RT chunks of the upstream gradient
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
@@ -647,7 +675,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(2
   const uint32_t dlane = dma_lane_offset(lane);
   const int wave = threadIdx.x / kWave;
   const int j = lane & 15, g = lane >> 4;
-  const int64_t q0 = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * (16 * QT);
+  const int64_t q0 = ((int64_t)blockIdx.x * WPB + wave) * (16 * QT);
   const int s_begin = blockIdx.y * steps_per_split;
   const int s_end = min(steps_total, s_begin + steps_per_split);
   out += blockIdx.y * part_stride;
