@@ -44,6 +44,14 @@
  *     fp32 accumulation after exact power-of-two scaling.  Each result is
  *     within 2e-3 (fp16 q,k) or 5e-3 (bf16 q,k) of sum_n Phi |v_n| per element
  *     of the exact value (and the analogous sums of |terms| for gradients).
+ *   - Domain of that bound: tau * ||q_m||^2 and tau * ||k_n||^2 at most 2^13
+ *     for all rows.  The fp32 exponent is formed from the expanded square, and
+ *     its rounding error grows as about tau * ||x||^2 * 2^-24 (relative error
+ *     of the result about 2.5e-4 at the limit, measured 6e-4 at 2.4 times
+ *     it).  Point sets far from the origin compared with their spread should
+ *     be centred on a common point by the caller first: Eq. 1 and its
+ *     gradients are invariant under a common translation of q and k (the
+ *     centring of Sec. 2, Remark 2).
  */
 #ifndef GAUSS_SUM_H
 #define GAUSS_SUM_H

@@ -190,7 +190,7 @@ SAMPLES = {
     "mmd_flow": (1024, 1024),
     "svgd": (1024, 1024),
     "mixture_d32": (1024, 1024),
-    "rect_d256": (96, 1024),
+    "rect_d256": (256, 1024),
 }
 
 
@@ -206,6 +206,11 @@ def test_workload_full_size_sampled_rows(name):
         _say("workload", name, "tau", w.tau, "full size", w.M, w.N)
         stats = parity.check_workload(w, rows=rows, key_rows=key_rows)
         _say("  stats", stats)
+        if name == "rect_d256":
+            # the query gradient on 1024 sampled rows (each against all 2^21 keys)
+            rows = wl.sample_rows(w.M, 1024, seed=3)
+            stats = parity.check_workload(w, passes=("dq",), rows=rows)
+            _say("  dq on 1024 rows", stats)
 
 
 def test_range_levels_plain_shifted_exact():
