@@ -441,6 +441,18 @@ DqK dq_for(const gs_problem& p, const Dims& dm, bool fused) {
 const void* fwd_kernel(const gs_problem& p, const Dims& dm) { return fwd_for(p, dm).kernel; }
 const void* dq_kernel(const gs_problem& p, const Dims& dm, bool fused) { return dq_for(p, dm, fused).kernel; }
 
+// Small forward problems: the preparation in one launch (k_prep_fwd_small)
+// and a row check that reads its key sample from the key copy, instead of
+// nine dependent launches.  Bounds: every workgroup of the preparation
+// reduces all N C values itself, and the point copies stay small.
+constexpr int64_t kSmallValues = 8192;        // N * C
+constexpr int64_t kSmallPointHalves = 1 << 18; // padded rows x RT width, per point set
+
+bool small_forward(const gs_problem& p, const Want& w, const Plan& pl, int64_t G) {
+  return w.fwd && !w.dq && !w.dk && !w.dv && G == 1 && p.N * p.C <= kSmallValues &&
+         pl.Mp * pl.dm.W() <= kSmallPointHalves && pl.Np * pl.dm.W() <= kSmallPointHalves;
+}
+
 // Lays out every buffer the requested passes need for one problem of a group
 // of G; with ws == nullptr only computes the size.
 void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& pl, int64_t G) {
@@ -678,26 +690,59 @@ void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64
 
 // Row-bound flags of the rows of `qs` (n rows, n_pad padded) against the
 // sampled keys of `ks`, stored after the sample's half norms.
-template <typename T>
-void row_check_t(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Side& ks) {
+template <typename T, bool GATHER>
+void row_check_t(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Side& ks, int64_t nk) {
   uint32_t* shift = reinterpret_cast<uint32_t*>(ks.samp_nh + kSampleRows);
   const dim3 grid = grid_g(c, (unsigned)(n_pad / 256)), block(kBlockThreads);
   const uint4* q = (const uint4*)qs.rt;
-  const uint4* s = (const uint4*)ks.samp_rt;
+  // the copied sample, or (GATHER) the key set's own RT copy and half norms
+  const uint4* s = (const uint4*)(GATHER ? ks.rt : ks.samp_rt);
+  const float* snh = GATHER ? ks.nh : ks.samp_nh;
   const Bz bz = bz_ws(c);
   switch (c.pl->dm.DP) {
-    case 1: hipLaunchKernelGGL((k_row_check<T, 1>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
-    case 2: hipLaunchKernelGGL((k_row_check<T, 2>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
-    case 4: hipLaunchKernelGGL((k_row_check<T, 4>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
-    case 8: hipLaunchKernelGGL((k_row_check<T, 8>), grid, block, 0, c.st, q, qs.nh, s, ks.samp_nh, c.tau2, n, shift, bz); break;
+    case 1: hipLaunchKernelGGL((k_row_check<T, 1, GATHER>), grid, block, 0, c.st, q, qs.nh, s, snh, c.tau2, n, shift, bz, nk); break;
+    case 2: hipLaunchKernelGGL((k_row_check<T, 2, GATHER>), grid, block, 0, c.st, q, qs.nh, s, snh, c.tau2, n, shift, bz, nk); break;
+    case 4: hipLaunchKernelGGL((k_row_check<T, 4, GATHER>), grid, block, 0, c.st, q, qs.nh, s, snh, c.tau2, n, shift, bz, nk); break;
+    case 8: hipLaunchKernelGGL((k_row_check<T, 8, GATHER>), grid, block, 0, c.st, q, qs.nh, s, snh, c.tau2, n, shift, bz, nk); break;
   }
 }
 
-void row_check(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Side& ks) {
-  if (c.p->qk_dtype == GS_F16)
-    row_check_t<F16>(c, qs, n, n_pad, ks);
+// Row-bound flags of the rows of qs against the key sample of ks; gather:
+// read the sampled keys from ks's own RT copy (nk keys) instead of a copy.
+void row_check(const Ctx& c, const Side& qs, int64_t n, int64_t n_pad, const Side& ks, bool gather = false,
+               int64_t nk = 0) {
+  if (c.p->qk_dtype == GS_F16) {
+    if (gather)
+      row_check_t<F16, true>(c, qs, n, n_pad, ks, nk);
+    else
+      row_check_t<F16, false>(c, qs, n, n_pad, ks, nk);
+  } else {
+    if (gather)
+      row_check_t<BF16, true>(c, qs, n, n_pad, ks, nk);
+    else
+      row_check_t<BF16, false>(c, qs, n, n_pad, ks, nk);
+  }
+}
+
+void prep_fwd_small(const Ctx& c, const void* q, const void* k, const void* v, bool alias) {
+  const gs_problem& p = *c.p;
+  Plan& pl = *c.pl;
+  const int W = pl.dm.W(), R = pl.dm.Rv();
+  const int64_t items = pl.Mp * (W / 8) + (alias ? 0 : pl.Np * (W / 8)) + (pl.Np / 32) * R * 4 + pl.Np;
+  const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(items, 256), 1024);
+  auto vec = [&](const void* x) {
+    return (int)((p.D % 8 == 0) && (reinterpret_cast<uintptr_t>(x) % 16 == 0));
+  };
+  const uint16_t* q16 = static_cast<const uint16_t*>(q);
+  const uint16_t* k16 = static_cast<const uint16_t*>(k);
+  if (p.qk_dtype == GS_F16)
+    hipLaunchKernelGGL(k_prep_fwd_small<F16>, dim3(blocks), dim3(256), 0, c.st, q16, k16, (int)alias, v,
+                       (int)p.v_dtype, p.M, p.N, (int)p.D, (int)p.C, pl.Mp, pl.Np, W, R, vec(q), vec(k), c.tau2,
+                       pl.q.rt, pl.q.nh, pl.k.rt, pl.k.nh, pl.v.ks, pl.scal_kv, pl.slots);
   else
-    row_check_t<BF16>(c, qs, n, n_pad, ks);
+    hipLaunchKernelGGL(k_prep_fwd_small<BF16>, dim3(blocks), dim3(256), 0, c.st, q16, k16, (int)alias, v,
+                       (int)p.v_dtype, p.M, p.N, (int)p.D, (int)p.C, pl.Mp, pl.Np, W, R, vec(q), vec(k), c.tau2,
+                       pl.q.rt, pl.q.nh, pl.k.rt, pl.k.nh, pl.v.ks, pl.scal_kv, pl.slots);
 }
 
 // Split partials (in the workspace slices) -> out (byte stride out_stride).
@@ -1165,6 +1210,12 @@ gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void*
     float* dv_ = at_o(dv, g0, dvs);
     if (p->qk_dtype == GS_F32) {
       run_f32(c, q_, qs, k_, ks, v_, vst, out_, os);
+      continue;
+    }
+    if (small_forward(*p, w, pl, G)) {
+      prep_fwd_small(c, q_, k_, v_, alias);
+      row_check(c, pl.q, M, pl.Mp, pl.k, true, N);
+      pass_fwd(c, pl.q, M, pl.k, N, pl.scal_kv, pl.v.ks, pl.slots + 0, out_, os);
       continue;
     }
     hipLaunchKernelGGL(k_fill_u32, grid_g(c, 1), dim3(64), 0, stream, pl.slots, 16, 0u, bz_ws(c));

@@ -256,10 +256,28 @@ __device__ __forceinline__ bool needs_shift(const uint4* __restrict__ sample_rt,
 // small sample; the full-sample maximum is never below the coarse one, so rows
 // passing the coarse check pass the full one).  The forward kernel reads these
 // flags.
-template <typename T, int DP>
+// Key row of sample position pos (coarse positions first, as k_sample
+// stores them): rows floor(j N / kSampleRows).
+__device__ __forceinline__ int64_t sample_row(int pos, int64_t n) {
+  constexpr int kStride = kSampleRows / kSampleCoarse;
+  int j;
+  if (pos < kSampleCoarse) {
+    j = kStride * pos;
+  } else {
+    const int q = pos - kSampleCoarse;
+    j = (q / (kStride - 1)) * kStride + q % (kStride - 1) + 1;
+  }
+  return ((int64_t)j * n) / kSampleRows;
+}
+
+// GATHER: the sample is not copied; sample_rt / sample_nh are then the key
+// set's own RT copy and half norms (nk > 0 keys), and the sampled rows are
+// read from there (the same values k_sample would copy).
+template <typename T, int DP, bool GATHER>
 __global__ __launch_bounds__(kBlockThreads) void k_row_check(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ sample_rt,
-    const float* __restrict__ sample_nh, float tau2, int64_t M, uint32_t* __restrict__ shift, Bz bz) {
+    const float* __restrict__ sample_nh, float tau2, int64_t M, uint32_t* __restrict__ shift, Bz bz,
+    int64_t nk) {
   constexpr int QT = 4;
   qs = zoff(qs, bz.ws);
   nhq = zoff(nhq, bz.ws);
@@ -280,8 +298,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_row_check(
   auto scan = [&](int t0, int t1) {
     for (int t = t0; t < t1; ++t) {
       uint4 kr[DP];
-      load_k_tile<DP>(sample_rt, t, j, g, kr);
-      const floatx4 cin = *reinterpret_cast<const floatx4*>(sample_nh + 16 * t + 4 * g);
+      floatx4 cin;
+      if constexpr (GATHER) {
+        const int64_t r = sample_row(16 * t + j, nk);
+#pragma unroll
+        for (int dc = 0; dc < DP; ++dc) kr[dc] = sample_rt[(((r >> 4) * DP + dc) * 16 + (r & 15)) * 4 + g];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) cin[u] = sample_nh[sample_row(16 * t + 4 * g + u, nk)];
+      } else {
+        load_k_tile<DP>(sample_rt, t, j, g, kr);
+        cin = *reinterpret_cast<const floatx4*>(sample_nh + 16 * t + 4 * g);
+      }
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) smax[qt] = max_into(smax[qt], score_tile<T, DP>(kr, qreg[qt], cin));
     }

@@ -113,17 +113,15 @@ __global__ void k_absmax(const void* __restrict__ x, int64_t count, int dtype,
 // size, so every lane of a wave runs the same iterations of the grid-stride
 // loop and the shuffles see whole waves.  vec: rows start on 16-byte
 // boundaries and D is a multiple of 8, so the eight columns are one 16-byte
-// load.
+// load.  rt_norm_item is one thread's share: item t (row t / cpr, columns
+// 8 (t % cpr) .. +7); it returns the row's half norm (the same value in
+// every lane of the row).
 template <typename T>
-__global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad,
-                                 int W, uint16_t* __restrict__ xs, float* __restrict__ nh, int vec,
-                                 Bz bz) {
-  x = zoff(x, bz.in);
-  xs = zoff(xs, bz.ws);
-  nh = zoff(nh, bz.ws);
+__device__ __forceinline__ float rt_norm_item(const uint16_t* __restrict__ x, int64_t n, int D, int W,
+                                              uint16_t* __restrict__ xs, float* __restrict__ nh, int vec,
+                                              int64_t t) {
   const int cpr = W >> 3;  // threads per row (4, 8, 16 or 32)
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * cpr; t += stride) {
+  {
     const int64_t r = t / cpr;
     const int c = (int)(t - r * cpr);
     uint16_t h[8];
@@ -153,8 +151,23 @@ __global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int 
     pk.z = h[4] | ((uint32_t)h[5] << 16);
     pk.w = h[6] | ((uint32_t)h[7] << 16);
     *reinterpret_cast<uint4*>(xs + rt_index(r, 8 * c, W)) = pk;
-    if (c == 0) nh[r] = r < n ? (float)(-0.5 * acc) : kPadBias;
+    const float half = r < n ? (float)(-0.5 * acc) : kPadBias;
+    if (c == 0) nh[r] = half;
+    return half;
   }
+}
+
+template <typename T>
+__global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int D, int64_t n_pad,
+                                 int W, uint16_t* __restrict__ xs, float* __restrict__ nh, int vec,
+                                 Bz bz) {
+  x = zoff(x, bz.in);
+  xs = zoff(xs, bz.ws);
+  nh = zoff(nh, bz.ws);
+  const int cpr = W >> 3;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * cpr; t += stride)
+    (void)rt_norm_item<T>(x, n, D, W, xs, nh, vec, t);
 }
 
 // Points, KS-layout fp16 copy scaled by 2^e (e from *slot when slot != NULL,
@@ -219,16 +232,9 @@ __global__ void k_values_rt(const void* __restrict__ v, int dtype, int64_t n, in
 // through the step scalars) row 0 holds sign(v) = +-1 instead.  Thread
 // (32-key block, row w, quarter a) writes the eight key slots 8a .. 8a+7 of
 // row w (one 16-byte store), as k_points_ks.
-__global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, int C, int64_t n_pad,
-                            int R, const uint32_t* __restrict__ slot, int sign_only,
-                            uint16_t* __restrict__ vt, Bz bz) {
-  v = zoff(v, bz.in);
-  slot = zoff(slot, bz.ws);
-  vt = zoff(vt, bz.ws);
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const float s = ldexpf(1.0f, scale_exponent(*slot));
-  const int64_t total = (n_pad >> 5) * R * 4;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
+__device__ __forceinline__ void values_ks_item(const void* __restrict__ v, int dtype, int64_t n, int C, int R,
+                                               float s, int sign_only, uint16_t* __restrict__ vt, int64_t t) {
+  {
     const int a = (int)(t & 3);
     const int64_t rest = t >> 2;
     const int64_t blk = rest / R;
@@ -249,6 +255,19 @@ __global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, in
     pk.w = h[6] | ((uint32_t)h[7] << 16);
     *reinterpret_cast<uint4*>(vt + ((blk * R + w) * 32 + 8 * a)) = pk;
   }
+}
+
+__global__ void k_values_ks(const void* __restrict__ v, int dtype, int64_t n, int C, int64_t n_pad,
+                            int R, const uint32_t* __restrict__ slot, int sign_only,
+                            uint16_t* __restrict__ vt, Bz bz) {
+  v = zoff(v, bz.in);
+  slot = zoff(slot, bz.ws);
+  vt = zoff(vt, bz.ws);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const float s = ldexpf(1.0f, scale_exponent(*slot));
+  const int64_t total = (n_pad >> 5) * R * 4;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride)
+    values_ks_item(v, dtype, n, C, R, s, sign_only, vt, t);
 }
 
 // Row-bound sample of a point set: rows n_j = floor(j N / kSampleRows) for
@@ -291,6 +310,29 @@ __global__ void k_sample(const uint16_t* __restrict__ x, int64_t n, int D, int W
 //            order (the order of the MFMA B operand built from two score
 //            tiles), two per float; otherwise 0;
 //   [48, 64) unused, 0.
+// Entry i < 32 of a step's scalars: the key bias of key r from its half
+// norm (plus log2 |v_r sc| / tau' for single-channel values v != NULL).
+__device__ __forceinline__ float key_bias(float half, const void* __restrict__ v, int dtype, int64_t n,
+                                          int64_t r, float sc, float tau2) {
+  float val = half;
+  if (v && r < n) val += log2f(fabsf(load_any(v, r, dtype) * sc)) / tau2;
+  return val;
+}
+// Entry i in [32, 64) of the scalars of step s: two fp16 signs of v in key-slot
+// order for i < 48 and single-channel values (v != NULL), else 0.
+__device__ __forceinline__ float step_sign_word(const void* __restrict__ v, int dtype, int64_t n, int64_t s,
+                                                int i) {
+  if (i >= 48 || !v) return 0.0f;
+  uint32_t bits = 0;
+  for (int h = 0; h < 2; ++h) {
+    const int z = 2 * (i - 32) + h;
+    const int64_t r = s * 32 + 16 * ((z & 7) >> 2) + 4 * (z >> 3) + (z & 3);
+    const bool neg = r < n && load_any(v, r, dtype) < 0.0f;
+    bits |= (neg ? 0xBC00u : 0x3C00u) << (16 * h);
+  }
+  return __builtin_bit_cast(float, bits);
+}
+
 __global__ void k_step_scalars(const float* __restrict__ nh, const void* __restrict__ v, int dtype,
                                int64_t n, int64_t n_pad, const uint32_t* __restrict__ slot, float tau2,
                                float* __restrict__ out, Bz bz) {
@@ -303,22 +345,69 @@ __global__ void k_step_scalars(const float* __restrict__ nh, const void* __restr
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_pad * 2; t += stride) {
     const int64_t s = t >> 6;
     const int i = (int)(t & 63);
-    float val = 0.0f;
-    if (i < 32) {
-      const int64_t r = s * 32 + i;
-      val = nh[r];
-      if (v && r < n) val += log2f(fabsf(load_any(v, r, dtype) * sc)) / tau2;
-    } else if (i < 48 && v) {
-      uint32_t bits = 0;
-      for (int h = 0; h < 2; ++h) {
-        const int z = 2 * (i - 32) + h;
-        const int64_t r = s * 32 + 16 * ((z & 7) >> 2) + 4 * (z >> 3) + (z & 3);
-        const bool neg = r < n && load_any(v, r, dtype) < 0.0f;
-        bits |= (neg ? 0xBC00u : 0x3C00u) << (16 * h);
-      }
-      val = __builtin_bit_cast(float, bits);
+    out[t] = i < 32 ? key_bias(nh[s * 32 + i], v, dtype, n, s * 32 + i, sc, tau2)
+                    : step_sign_word(v, dtype, n, s, i);
+  }
+}
+
+// All per-call preparation of a small forward problem in one launch (the
+// chain fill / |v| maximum / copies / scalars takes nine dependent launches
+// of a few microseconds each otherwise): every workgroup first reduces
+// max |v| over all N x C values itself (no atomics, nothing to clear; the
+// caller keeps N C small), then the grid-stride items are, in order, the RT
+// copy and half norms of q (segment A), of k with the first 32 step scalars
+// of each key (B; skipped when q and k are the same array), the KS copy of
+// the values (C) and the sign words of the step scalars (D).  Segment lengths
+// are multiples of the wave size, so the lanes of a point row stay in one
+// wave.  slot receives max |v| (as gauss_sum's prep would write it).  The
+// results are bitwise those of the separate kernels.
+template <typename T>
+__global__ __launch_bounds__(256) void k_prep_fwd_small(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int alias, const void* __restrict__ v,
+    int vdt, int64_t M, int64_t N, int D, int C, int64_t Mp, int64_t Np, int W, int R, int vecq, int veck,
+    float tau2, uint16_t* __restrict__ qrt, float* __restrict__ qnh, uint16_t* __restrict__ krt,
+    float* __restrict__ knh, uint16_t* __restrict__ vks, float* __restrict__ scal,
+    uint32_t* __restrict__ slot) {
+  __shared__ uint32_t wmax[256 / kWave];
+  uint32_t mb = 0;
+  for (int64_t i = threadIdx.x; i < N * C; i += blockDim.x) {
+    const uint32_t b = __builtin_bit_cast(uint32_t, fabsf(load_any(v, i, vdt)));
+    mb = b > mb ? b : mb;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t o = (uint32_t)__shfl_xor((int)mb, off, kWave);
+    mb = o > mb ? o : mb;
+  }
+  if ((threadIdx.x & (kWave - 1)) == 0) wmax[threadIdx.x / kWave] = mb;
+  __syncthreads();
+  mb = wmax[0];
+  for (int w = 1; w < (int)(blockDim.x / kWave); ++w) mb = wmax[w] > mb ? wmax[w] : mb;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *slot = mb;
+  const int e = scale_exponent(mb);
+  const float sv = ldexpf(1.0f, e);                           // values (KS copy)
+  const void* v1 = C == 1 ? v : nullptr;                      // single channel: |v| in the scalars
+  const float sc = v1 ? ldexpf(1.0f, e - 1) : 0.0f;
+  const int cpr = W >> 3;
+  const int64_t nA = Mp * cpr, nB = alias ? 0 : Np * cpr, nC = (Np >> 5) * R * 4, nD = Np;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nA + nB + nC + nD; t += stride) {
+    if (t < nA) {
+      const float half = rt_norm_item<T>(q, M, D, W, qrt, qnh, vecq, t);
+      const int64_t r = t / cpr;
+      if (alias && t - r * cpr == 0) scal[(r >> 5) * 64 + (r & 31)] = key_bias(half, v1, vdt, N, r, sc, tau2);
+    } else if (t < nA + nB) {
+      const int64_t u = t - nA;
+      const float half = rt_norm_item<T>(k, N, D, W, krt, knh, veck, u);
+      const int64_t r = u / cpr;
+      if (u - r * cpr == 0) scal[(r >> 5) * 64 + (r & 31)] = key_bias(half, v1, vdt, N, r, sc, tau2);
+    } else if (t < nA + nB + nC) {
+      values_ks_item(v, vdt, N, C, R, sv, C == 1, vks, t - nA - nB);
+    } else {
+      const int64_t u = t - nA - nB - nC;
+      const int64_t s = u >> 5;
+      const int i = 32 + (int)(u & 31);
+      scal[s * 64 + i] = step_sign_word(v1, vdt, N, s, i);
     }
-    out[t] = val;
   }
 }
 
