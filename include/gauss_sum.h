@@ -255,8 +255,9 @@ size_t gauss_sum_mmd_flow_workspace_size(const gs_problem* p);
  *   phi[m, :] = sum_n Phi(x_m, x_n) score_n + tau sum_n Phi(x_m, x_n) (x_m - x_n)
  * (fp32, N x D), the SVGD direction without its 1/N factor (the second sum is
  * the gradient of sum_n Phi(x_n, x_m) with respect to x_n, summed: the
- * repulsive term).  Computed as the forward sum with values score and the
- * query-gradient pass with unit weights.  Requires p->M == p->N and
+ * repulsive term).  One pass over the pairs: the kernel values are formed
+ * once and feed both the sum with values score and the query gradient with
+ * unit weights (their difference is written).  Requires p->M == p->N and
  * p->C == p->D (GS_ERR_BAD_SHAPE); fp16 or bf16 points.  phi must not overlap
  * x, score or the workspace.  N == 0 is a no-op.  Workspace:
  * gauss_sum_svgd_workspace_size. */

@@ -226,6 +226,47 @@ DqK dq_fn(int DP, int CW, int CT, bool fused) {
   return {};
 }
 
+// SVGD direction in one pass (k_dq with SV = true, C = D): query tiles per
+// wave so that the query operands, dQ and the forward accumulators stay
+// within the register budget.
+constexpr int sv_qt(int DP) { return DP == 8 ? 1 : DP == 4 ? 2 : 4; }
+
+using SvFn = void (*)(dim3, hipStream_t, const uint4*, const float*, const uint4*, const float*,
+                      const uint4*, const float*, const uint4*, const uint32_t*, const uint32_t*, float,
+                      float, int64_t, int, int, int, float*, int64_t, const uint4*);
+
+template <typename T, int DP, int CT>
+void launch_sv(dim3 grid, hipStream_t st, const uint4* xs, const float* nh, const uint4* srt,
+               const float* snh, const uint4* ks, const float* scal, const uint4* kt, const uint32_t* kslot,
+               const uint32_t* vslot, float tau2, float tau, int64_t M, int D, int steps, int sps, float* out,
+               int64_t pstride, const uint4* vt) {
+  hipLaunchKernelGGL((k_dq<T, DP, 0, sv_qt(DP), CT, false, dq_wpb(DP), true>), grid, dim3(kWave * dq_wpb(DP)), 0,
+                     st, xs, nh, srt, snh, ks, scal, kt, kslot, nullptr, vslot, nullptr, nullptr, nullptr, 0,
+                     tau2, tau, M, D, steps, sps, out, pstride, vt, D, nullptr, 0, Bz{});
+}
+
+struct SvK {
+  SvFn launch = nullptr;
+  const void* kernel = nullptr;
+};
+
+template <typename T, int DP, int CT>
+SvK sv_k() {
+  return {&launch_sv<T, DP, CT>,
+          reinterpret_cast<const void*>(&k_dq<T, DP, 0, sv_qt(DP), CT, false, dq_wpb(DP), true>)};
+}
+
+// The instance for D (CT = 16-row tiles of C = D).
+template <typename T>
+SvK sv_fn(int DP, int CT) {
+  if (DP == 1 && CT == 1) return sv_k<T, 1, 1>();
+  if (DP == 1 && CT == 2) return sv_k<T, 1, 2>();
+  if (DP == 2 && CT == 4) return sv_k<T, 2, 4>();
+  if (DP == 4 && CT == 8) return sv_k<T, 4, 8>();
+  if (DP == 8 && CT == 16) return sv_k<T, 8, 16>();
+  return {};
+}
+
 // fp32 tier (fp32 points, C = 1, forward): the kernel for D chunks DP.
 const void* f32_kernel(int DP) {
   switch (DP) {
@@ -1331,24 +1372,58 @@ gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, c
 
 // SVGD: workspace = unit weights (N floats) and the query-gradient buffer
 // (N x D floats), then room for the larger of the two passes.
-size_t svgd_extra(int64_t n, int64_t D) {
-  return (size_t)(gs::round_up(std::max<int64_t>(n, 1) * 4, 256) +
-                  gs::round_up(std::max<int64_t>(n, 1) * D * 4, 256));
+}  // extern "C"
+
+namespace gs {
+namespace {
+
+// Workspace of gauss_sum_svgd: the point-side arrays of a unit-weight dq
+// pass (RT copy, half norms, KS copy, sample, key scalars), the KS copy of
+// the scores, and the split partials of the one SVGD pass.
+struct SvPlan {
+  gs_problem p1;  // the problem with C = 1 (unit weights) whose plan holds the point side
+  Plan pl;
+  Dims dm;        // tiles for C = D
+  SvK k;
+  PassShape ps;
+  uint16_t* score_ks = nullptr;
+  float* part = nullptr;
+  size_t total = 0;
+};
+
+void svgd_plan(const gs_problem& p, void* ws, SvPlan& sp) {
+  sp.p1 = p;
+  sp.p1.C = 1;
+  sp.p1.v_dtype = GS_F32;
+  make_plan(sp.p1, want_for(sp.p1, false, true, false, false), true, ws, sp.pl, 1);
+  Carver cv;
+  cv.base = static_cast<char*>(ws);
+  cv.off = sp.pl.total;
+  sp.dm = dims_of(p.D, p.D);
+  sp.k = p.qk_dtype == GS_F16 ? sv_fn<F16>(sp.dm.DP, sp.dm.CT) : sv_fn<BF16>(sp.dm.DP, sp.dm.CT);
+  sp.score_ks = cv.take<uint16_t>(sp.pl.Np * sp.dm.Rv() * 2);
+  sp.ps = pass_shape(p.N, p.N, sv_qt(sp.dm.DP), sp.k.kernel, 1, dq_wpb(sp.dm.DP));
+  sp.part = sp.ps.splits > 1 ? cv.take<float>((size_t)sp.ps.splits * p.N * p.D * 4) : nullptr;
+  sp.total = cv.off;
 }
-gs_problem svgd_flow_problem(const gs_problem* p) {
-  gs_problem q = *p;
-  q.C = 1;
-  q.v_dtype = GS_F32;
-  return q;
-}
+
+}  // namespace
+}  // namespace gs
+
+extern "C" {
+
 size_t gauss_sum_svgd_workspace_size(const gs_problem* p) {
   if (!p || gs::check_problem(p) != GS_SUCCESS || p->M != p->N || p->C != p->D ||
       p->qk_dtype == GS_F32 || p->N == 0)
     return 0;
-  const gs_problem q = svgd_flow_problem(p);
-  return svgd_extra(p->N, p->D) +
-         std::max(gs::workspace_for(p, true, 0, 0, 0), gs::workspace_for(&q, false, 1, 0, 0));
+  gs::SvPlan sp;
+  gs::svgd_plan(*p, nullptr, sp);
+  return sp.total;
 }
+
+// One pass over the pairs: k_dq in its SVGD mode forms the kernel values
+// once and accumulates both the score sum (values = scores) and the unit-
+// weight query gradient, and writes their difference.
 gs_status gauss_sum_svgd(const gs_problem* p, const void* x, const void* score, float tau, float* phi,
                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
   using namespace gs;
@@ -1361,30 +1436,41 @@ gs_status gauss_sum_svgd(const gs_problem* p, const void* x, const void* score, 
     if (!phi) return GS_ERR_NULL_POINTER;
     const int64_t n = p->N, D = p->D;
     if (n > 0 && (!x || !score)) return GS_ERR_NULL_POINTER;
-    if (!aligned(phi, 4)) return GS_ERR_MISALIGNED;
+    if (!aligned(phi, 4) || (n > 0 && (!aligned(x, 2) || !aligned(score, dsize(p->v_dtype)))))
+      return GS_ERR_MISALIGNED;
     if (n == 0) return GS_SUCCESS;
-    const size_t need = gauss_sum_svgd_workspace_size(p);
-    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_SUCCESS) return st;
+    SvPlan sp;
+    svgd_plan(*p, nullptr, sp);
+    if (!sp.k.launch) return GS_ERR_INTERNAL;
+    if ((st = check_workspace(workspace, workspace_bytes, sp.total)) != GS_SUCCESS) return st;
     const Range in[3] = {range_of(x, n * D * 2), range_of(score, n * D * (int64_t)dsize(p->v_dtype)),
-                         range_of(workspace, (int64_t)need)};
+                         range_of(workspace, (int64_t)sp.total)};
     for (int b = 0; b < 3; ++b)
       if (overlap(range_of(phi, n * D * 4), in[b])) return GS_ERR_ALIAS;
-    char* base = static_cast<char*>(workspace);
-    float* ones = reinterpret_cast<float*>(base);
-    float* flow = reinterpret_cast<float*>(base + round_up(std::max<int64_t>(n, 1) * 4, 256));
-    const size_t extra = svgd_extra(n, D);
-    // phi = sum_n Phi(x_m, x_n) score_n
-    st = run(p, nullptr, x, x, score, tau, nullptr, GS_F32, phi, nullptr, nullptr, nullptr, base + extra,
-             workspace_bytes - extra, stream);
-    if (st != GS_SUCCESS) return st;
-    // flow = tau sum_n Phi (x_n - x_m): the query gradient with unit weights
-    // and unit upstream gradient
-    const gs_problem q = svgd_flow_problem(p);
-    hipLaunchKernelGGL(k_fill_f32, dim3(grid1(n)), dim3(256), 0, stream, ones, n, 1.0f);
-    st = run(&q, nullptr, x, x, ones, tau, ones, GS_F32, nullptr, flow, nullptr, nullptr, base + extra,
-             workspace_bytes - extra, stream);
-    if (st != GS_SUCCESS) return st;
-    hipLaunchKernelGGL(k_sub_f32, dim3(grid1(n * D)), dim3(256), 0, stream, phi, (const float*)flow, n * D);
+    svgd_plan(*p, workspace, sp);
+    Plan& pl = sp.pl;
+    const float tau2 = (float)(tau * 1.4426950408889634);
+    Ctx c{stream, &sp.p1, &pl, tau, tau2, 1u, (int64_t)pl.total};
+    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(64), 0, stream, pl.slots, 16, 0u, Bz{});
+    // points: RT copy, half norms, sample, KS copy (plain: unit weights)
+    prep_points(c, x, 0, n, pl.Mp, pl.q, pl.slots + 2);
+    // scores: |max| and the KS copy (the values of the forward sum)
+    hipLaunchKernelGGL(k_absmax, dim3(grid_reduce(n * D)), dim3(256), 0, stream, score, n * D,
+                       (int)p->v_dtype, pl.slots + 0, Bz{});
+    hipLaunchKernelGGL(k_values_ks, dim3(grid1(pl.Np / 8 * sp.dm.Rv())), dim3(256), 0, stream, score,
+                       (int)p->v_dtype, n, (int)D, pl.Np, sp.dm.Rv(), (const uint32_t*)pl.slots + 0, 0,
+                       sp.score_ks, Bz{});
+    // key scalars: half norms only (unit weights)
+    prep_scalars(c, pl.q, nullptr, GS_F32, 0, n, pl.Np, pl.slots + 0, pl.scal_kv);
+    const PassShape& ps = sp.ps;
+    const bool split = ps.splits > 1;
+    prof_before(kKindGrad, stream);
+    sp.k.launch(dim3(ps.blocks, ps.splits), stream, (const uint4*)pl.q.rt, pl.q.nh, (const uint4*)pl.q.samp_rt,
+                pl.q.samp_nh, (const uint4*)pl.q.rt, pl.scal_kv, (const uint4*)pl.q.ks,
+                p->qk_dtype == GS_BF16 ? pl.slots + 2 : nullptr, pl.slots + 0, tau2, tau, n, (int)D, ps.steps,
+                ps.sps, split ? sp.part : phi, split ? n * D : 0, (const uint4*)sp.score_ks);
+    prof_after(kKindGrad, stream);
+    combine(c, ps, sp.part, n * D, phi, 0);
     return launch_status();
   } catch (...) {
     return GS_ERR_INTERNAL;

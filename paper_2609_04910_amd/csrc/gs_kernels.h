@@ -656,7 +656,14 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
 // per CU: the large-D / large-C instances would otherwise take a few more
 // registers and run one wave per SIMD, which costs far more than the spill
 // of a few values outside the key loop.
-template <typename T, int DP, int CW, int QT, int FCT, bool BZ, int WPB>
+//
+// SV (with CW = 0): the SVGD direction of Sec. 3 in one pass.  Unit weights
+// (P = Phi, no value magnitudes in the step scalars, no signs in the key
+// copy), the FCT 16-row tiles of V^T hold the scores (C = D), and the
+// epilogue writes out = sum_n Phi score_n - tau sum_n Phi (k_n - q_m) (the
+// forward sum minus the query gradient with unit weights), or its split
+// partial.
+template <typename T, int DP, int CW, int QT, int FCT, bool BZ, int WPB, bool SV = false>
 __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))) void k_dq(
     const uint4* __restrict__ qs, const float* __restrict__ nhq, const uint4* __restrict__ samp_rt,
     const float* __restrict__ samp_nh, const uint4* __restrict__ ks, const float* __restrict__ scal,
@@ -688,7 +695,8 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   constexpr int KCH = 2 * DP;               // chunks of K (RT) per step
   constexpr int VCH = 2 * CW;               // chunks of V (RT) per step
   constexpr int TCH = DT;                   // chunks of K^T (KS) per step: 32 DP rows x 64 B
-  constexpr int FCH = CW > 0 ? FCT : 0;     // chunks of V^T (KS) per step, fused forward
+  static_assert(!SV || CW == 0, "SVGD mode uses unit weights");
+  constexpr int FCH = (CW > 0 || SV) ? FCT : 0;  // chunks of V^T (KS) per step, fused forward
   constexpr int NCH = KCH + VCH + TCH + FCH;
   constexpr int STAGE = NCH * 1024 + kScalarFloats * 4;
   // eight waves (one workgroup per CU): waves 0-3 copy every chunk, waves 4-7
@@ -780,8 +788,8 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
       if constexpr (CW > 0) load_k_tile_lds<GW>(vb, kt, j, g, vr[kt]);
     }
     // per key slot of this lane's B operand: sign(v_n) (single channel) or 1
-    const uint4 sg = CW > 0 ? uint4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u}
-                            : *reinterpret_cast<const uint4*>(sc + 32 + 4 * g);
+    const uint4 sg = (CW > 0 || SV) ? uint4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u}
+                                    : *reinterpret_cast<const uint4*>(sc + 32 + 4 * g);
     uint4 ktr[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + j) * 4 + lds_col(j, g)];
@@ -819,6 +827,10 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
       for (int qt = 0; qt < QT; ++qt) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) dQ[qt][dt] = mfma_f16(ktr[dt], b[qt], dQ[qt][dt]);
+        if constexpr (SV) {
+#pragma unroll
+          for (int ct = 0; ct < FCH; ++ct) O[qt][ct] = mfma_f16(vtr[ct], b[qt], O[qt][ct]);
+        }
         if constexpr (DP > 1) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
       }
       return;
@@ -863,6 +875,36 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   for (int qt = 0; qt < QT; ++qt) {
     rs[qt] += __shfl_xor(rs[qt], 16, kWave);
     rs[qt] += __shfl_xor(rs[qt], 32, kWave);
+  }
+  if constexpr (SV) {
+    // SVGD direction: the forward sum over the scores (scaled by 2^ev in their
+    // copy) minus the unit-weight query gradient tau (sum_n Phi k_n - q_m sum_n Phi)
+    const int ev = scale_exponent(*vslot);
+    const bool v4d = vec4_rows(out, D);
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      const int64_t m = q0 + 16 * qt + j;
+      if (m >= M) continue;
+      const float fo = exp2f(off[qt]);
+      const float fw = tau * fo;
+      const float rm = rs[qt];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int d0 = 16 * dt + 4 * g;
+        if (d0 >= D) continue;
+        const uint2 qq = *reinterpret_cast<const uint2*>(q16 + rt_index(m, d0, 32 * DP));
+        const float qv[4] = {T::to_float((uint16_t)qq.x), T::to_float((uint16_t)(qq.x >> 16)),
+                             T::to_float((uint16_t)qq.y), T::to_float((uint16_t)(qq.y >> 16))};
+        float o[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float fwd = dt < FCH ? ldexpf(O[qt][dt < FCH ? dt : 0][r], -ev) * fo : 0.0f;
+          o[r] = fwd - (ldexpf(dQ[qt][dt][r], -ek) - qv[r] * rm) * fw;
+        }
+        store_row4(out + m * D, d0, D, v4d, o[0], o[1], o[2], o[3]);
+      }
+    }
+    return;
   }
   if constexpr (FCT > 0) {
     // fused forward output: single channel from the signed row sums (values

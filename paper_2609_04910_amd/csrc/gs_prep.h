@@ -27,14 +27,6 @@ __global__ void k_fill_f32(float* __restrict__ p, int64_t n, float val) {
   for (; i < n; i += stride) p[i] = val;
 }
 
-// out[i] -= sub[i] for i < n (the SVGD update: kernel-weighted scores minus
-// the query-gradient pass with unit weights).
-__global__ void k_sub_f32(float* __restrict__ out, const float* __restrict__ sub, int64_t n) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (; i < n; i += stride) out[i] -= sub[i];
-}
-
 
 // max |x| over count elements into *slot (float bits; |x| >= 0 so unsigned
 // comparison of the bit patterns orders them; NaN compares largest).  Reduced
