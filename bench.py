@@ -28,7 +28,8 @@ measured with the library's event hook over the same timed steps.  The fp64
 CPU oracle is timed on a bounded sample of query rows of the same workload
 (rank 0, one GPU only).
 
-roofline.traffic: HBM bytes per launch of the dominant kernel, from the
+roofline.traffic: HBM bytes per launch of the dominant kernel (the mean over
+its dispatches, as for the launch time), from the
 rocprofv3 FETCH_SIZE and WRITE_SIZE counters (one --pmc run each), scaled by
 what the same counters read for a device copy of known size run in the same
 process (--calibrate-copy); recorded by --traffic-from into
@@ -142,7 +143,7 @@ def traffic_from(workload, fetch_dir, write_dir, copy_bytes, dominant):
         cpy = [v for name, vs in vals.items() if COPY_KERNEL_HINT in name.lower() for v in vs]
         if not dom or not cpy:
             raise SystemExit("traffic: no %s samples for %s / the copy kernel in %s" % (counter, dominant, d))
-        kib_dom = sorted(dom)[len(dom) // 2]          # median over dispatches
+        kib_dom = sum(dom) / len(dom)                 # mean over dispatches, as the launch time
         kib_cpy = max(cpy)                            # the calibration copies are the largest
         factor = copy_bytes / (kib_cpy * 1024.0)      # bytes moved per counted byte
         rec[key] = {"counter_kib_per_launch": kib_dom, "copy_counter_kib": kib_cpy,
@@ -295,7 +296,7 @@ def fused_passes(D, C):
     """Which forward-type sums the library computes inside a gradient launch
     (the fusion rule of gauss_sum_fwd_bwd): (forward inside the dq pass, dv
     inside the dk pass)."""
-    f = C == 1 or (C <= 16 and D <= 128)
+    f = C <= 16
     return f, f
 
 
@@ -730,10 +731,10 @@ def bench_batched_grad(args):
     ms_per_step = e0.elapsed_time(e1) / args.steps
     pairs = float(B) * M * N
     # gradient-kind launches per step: the dq pass (forward fused) and the dk
-    # pass (dv fused where the forward fusion applies: C = 1, or C <= 16 and D <= 128)
+    # pass (dv fused where the forward fusion applies: C <= 16)
     per_step = max(1, len(kernel_ms) // args.steps)
     grad_ms = float(np.sum(kernel_ms)) / args.steps if kernel_ms else float("nan")
-    fused_kv = C == 1 or (C <= 16 and D <= 128)
+    fused_kv = fused_passes(D, C)[1]
     # algorithmic flops per pair: a gradient pass with a forward-type sum fused
     # 4D+4C (4D+2C for the gradient, 2C more for the sum), else 4D+2C for dk
     # and a separate dv pass 2D+2C

@@ -147,8 +147,10 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
  * and any of dq, dk, dv (as gauss_sum_bwd, NULL = not requested) for the
  * given upstream gradient dout.  Sec. 3 of the paper observes that the query
  * gradient is itself one kernel sum over the same pairs (values (v_n k_n,
- * v_n)); with dq requested, the forward sum is produced by the same pass that
- * computes dq, so the kernel values are evaluated once for both.  Meant for
+ * v_n)); with dq requested and C <= 16, the forward sum is produced by the
+ * same pass that computes dq, so the kernel values are evaluated once for
+ * both (and with dk and dv requested, dv likewise rides in the dk pass; wider
+ * values get passes of their own).  Meant for
  * callers that know dout before the forward result (MMD flows use dout = v).
  * Results equal those of separate gauss_sum_fwd and gauss_sum_bwd calls to
  * within the stated tolerance. */

@@ -444,15 +444,15 @@ PassShape pass_shape(int64_t rows, int64_t keys, int QT, const void* kernel, int
 
 // When the forward sum rides along in the dq pass.  C = 1 always (it is the
 // row sum the gradient forms anyway).  Otherwise only while it needs a single
-// 16-row tile of V^T and D <= 128: beyond that the extra contraction and its
-// registers cost more than a separate forward pass (C = 128: 0.52 ms fused
-// against 0.17 + 0.25 ms; D = 256, C = 16: 598 ms against 112 + 388 ms).
+// 16-row tile of V^T: beyond that the extra contraction and its registers
+// cost more than a separate forward pass (C = 128, D = 128: 0.52 ms fused
+// against 0.17 + 0.25 ms).  At D = 256, C = 16 the fused passes take 276 +
+// 264 ms against 105 + 265 + 252 + 106 ms for the four separate ones.
 constexpr int64_t kFuseMaxC = 16;
-constexpr int64_t kFuseMaxD = 128;
 
 struct Want {
   bool fwd = false, dq = false, dk = false, dv = false;
-  bool fuse = false;  // set by want_for (kFuseMaxC, kFuseMaxD)
+  bool fuse = false;  // set by want_for (kFuseMaxC)
   bool fused() const { return fwd && dq && fuse; }  // forward computed inside the dq pass
   // dv computed inside the dk pass: with the roles of (q, dout) and (k, v)
   // exchanged, dv_n = sum_m Phi g_m is that pass's forward sum
@@ -465,7 +465,7 @@ Want want_for(const gs_problem& p, bool fwd, bool dq, bool dk, bool dv) {
   w.dq = dq;
   w.dk = dk;
   w.dv = dv;
-  w.fuse = p.C == 1 || (p.C <= kFuseMaxC && p.D <= kFuseMaxD);
+  w.fuse = p.C <= kFuseMaxC;
   return w;
 }
 

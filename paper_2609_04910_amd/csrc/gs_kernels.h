@@ -704,6 +704,13 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   constexpr bool WIDE = WPB == 2 * kWavesPerBlock;
   constexpr int NS = WIDE ? wide_stages(STAGE, NCH + 1) : ring_stages(STAGE, NCH + 1);
   constexpr int GW = CW > 0 ? CW : 1;       // RT chunks of the upstream gradient
+  // The fused forward at D > 128 (several channels): qreg (64) and dQ (128
+  // registers) leave too few for the step's operands when all of a tile's
+  // score operands are held across the query tiles; in three phases with the
+  // operands read as they are used the pass fits in 256 registers without
+  // spills in the key loop (and the forward costs a few per cent of the pass
+  // instead of a pass of its own)
+  constexpr bool PHASED = CW > 0 && FCH > 0 && DP >= 8;
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
@@ -784,17 +791,73 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
-      load_k_tile_lds<DP>(kb, kt, j, g, kr[kt]);
+      if constexpr (!PHASED) load_k_tile_lds<DP>(kb, kt, j, g, kr[kt]);
       if constexpr (CW > 0) load_k_tile_lds<GW>(vb, kt, j, g, vr[kt]);
     }
     // per key slot of this lane's B operand: sign(v_n) (single channel) or 1
     const uint4 sg = (CW > 0 || SV) ? uint4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u}
                                     : *reinterpret_cast<const uint4*>(sc + 32 + 4 * g);
+    const uint4* fb = reinterpret_cast<const uint4*>(base + (KCH + VCH + TCH) * 1024);
+    if constexpr (PHASED) {
+      // all score MFMAs (A operands read chunk by chunk, each feeding every
+      // query tile), then the w contractions, exponentials and products, then
+      // the contractions over keys with their A operands read as they are used
+      floatx4 acc[QT][2];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) acc[qt][kt] = cin[kt];
+      const int col = lds_col(j, g);
+#pragma unroll
+      for (int dc = 0; dc < DP; ++dc) {
+        const uint4 a0 = kb[(dc * 16 + j) * 4 + col];
+        const uint4 a1 = kb[((DP + dc) * 16 + j) * 4 + col];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          acc[qt][0] = mfma_qk<T>(a0, qreg[qt][dc], acc[qt][0]);
+          acc[qt][1] = mfma_qk<T>(a1, qreg[qt][dc], acc[qt][1]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      uint4 b[QT], bphi[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        float p[2][4], phi[2][4];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+          floatx4 w = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int cw = 0; cw < CW; ++cw) w = mfma_f16(vr[kt][cw], greg[qt][cw], w);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            phi[kt][r] = exp2_clamped(fmaf(acc[qt][kt][r], tau2, bq[qt]));
+            p[kt][r] = phi[kt][r] * w[r];
+          }
+        }
+        bphi[qt] = pack_tile_pair(phi);
+        b[qt] = pack_tile_pair(p);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ct = 0; ct < FCH; ++ct) {
+        const uint4 a = fb[(16 * ct + j) * 4 + col];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, bphi[qt], O[qt][ct]);
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const uint4 a = tb[(16 * dt + j) * 4 + col];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
+      }
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
+      return;
+    }
     uint4 ktr[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + j) * 4 + lds_col(j, g)];
     uint4 vtr[FCH > 0 ? FCH : 1];
-    const uint4* fb = reinterpret_cast<const uint4*>(base + (KCH + VCH + TCH) * 1024);
 #pragma unroll
     for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + j) * 4 + lds_col(j, g)];
     if constexpr (CW == 0) {

@@ -38,9 +38,9 @@ def test_traffic_record_roundtrip(tmp_path, monkeypatch):
     copy = 512 << 20
     fetch, write = str(tmp_path / "fetch"), str(tmp_path / "write")
     # the copy kernel reads half of its bytes in counter units (scale 2), the
-    # dominant kernel's median over dispatches is taken
-    _write_counters(fetch, "FETCH_SIZE", [("void gs::k_dq<x>", 100.0), ("void gs::k_dq<x>", 300.0),
-                                          ("void gs::k_dq<x>", 200.0), ("elementwise_copy_kernel", copy / 2048.0)])
+    # dominant kernel's mean over dispatches is taken (as for its launch time)
+    _write_counters(fetch, "FETCH_SIZE", [("void gs::k_dq<x>", 100.0), ("void gs::k_dq<x>", 400.0),
+                                          ("void gs::k_dq<x>", 100.0), ("elementwise_copy_kernel", copy / 2048.0)])
     _write_counters(write, "WRITE_SIZE", [("void gs::k_dq<x>", 50.0), ("elementwise_copy_kernel", copy / 1024.0)])
     bench.traffic_from("wl", fetch, write, copy, "k_dq")
     rec = json.load(open(tmp_path / "traffic_wl.json"))
@@ -88,8 +88,12 @@ def test_algorithmic_step_flops():
 
 
 def test_dominant_launch_flops_follow_the_fusion_rule():
-    # D = 256, C = 16: nothing fused; dq and dk launches 4D+2C each
-    assert bench.dominant_flops(("fwd", "dq", "dk", "dv"), 256, 16, True) == 4 * 256 + 2 * 16
+    # D = 256, C = 16: forward fused into dq, dv into dk; 4D+4C each
+    assert bench.dominant_flops(("fwd", "dq", "dk", "dv"), 256, 16, True) == 4 * 256 + 4 * 16
+    # separate calls: the forward has its own pass, dv still rides in dk
+    assert bench.dominant_flops(("fwd", "dq", "dk", "dv"), 256, 16, False) == 4 * 256 + 3 * 16
+    # C = 128: nothing fused; dq and dk launches 4D+2C each
+    assert bench.dominant_flops(("fwd", "dq", "dk", "dv"), 128, 128, True) == 4 * 128 + 2 * 128
     # single channel: forward fused into dq, dv into dk
     assert bench.dominant_flops(("fwd", "dq"), 64, 1, True) == 4 * 64 + 4
     assert bench.dominant_flops(("fwd", "dq"), 64, 1, False) == 4 * 64 + 2

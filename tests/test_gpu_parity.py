@@ -80,10 +80,10 @@ def test_same_points_alias_matches_separate_arrays():
     parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
 
 
-@pytest.mark.parametrize("D,C", [(24, 1), (40, 9), (128, 16), (130, 16), (64, 17)])
+@pytest.mark.parametrize("D,C", [(24, 1), (40, 9), (128, 16), (130, 16), (256, 16), (200, 3), (64, 17)])
 def test_dv_alone_and_fused_into_dk(D, C):
     """dv requested alone (its own forward-type pass) and together with dk
-    (where the forward fusion applies, C = 1 or C <= 16 and D <= 128, the dk
+    (where the forward fusion applies, C <= 16, the dk
     pass forms it as its forward sum): both match the oracle, and dk does not
     depend on whether dv rides along."""
     import torch
