@@ -531,7 +531,12 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   }
   const bool keys_k = w.fwd || w.dq;  // passes whose keys are k
   const bool keys_q = w.dk || w.dv;   // passes whose keys are q
-  const bool need_k_ks = w.dq, need_q_ks = w.dk;
+  // KS copies of the points: keys of a gradient pass, unless that pass reads
+  // its K^T operands from the RT tiles (dq_transposed_keys)
+  const bool f16 = p.qk_dtype == GS_F16;
+  const int cw = dq_cw(p, pl.dm);
+  const bool need_k_ks = w.dq && !dq_transposed_keys(f16, pl.dm.DP, cw, w.fused() ? 1 : 0);
+  const bool need_q_ks = w.dk && !dq_transposed_keys(f16, pl.dm.DP, cw, w.fused_kv() ? 1 : 0);
   // sample of a key side: its half norms are followed by the row-bound flags
   // of the rows queried against it (the other side's padded row count)
   auto side = [&](Side& s, int64_t n_pad, bool ks, bool sample, int64_t other_pad) {

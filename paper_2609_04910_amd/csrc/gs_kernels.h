@@ -397,6 +397,48 @@ __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
   return b;
 }
 
+// Whether the gradient kernel takes its K^T operands from the streamed RT
+// key tiles by transposing LDS reads instead of streaming a KS copy of the
+// keys: fp16 points only (the RT tiles then hold exactly the fp16 values the
+// contraction needs; a bf16 KS copy is converted to fp16), and only for the
+// three-phase step (several channels with a fused forward-type sum, D > 128).
+// The host planner uses the same rule to leave out the KS copy.
+constexpr bool dq_transposed_keys(bool f16_points, int DP, int CW, int FCT) {
+  return f16_points && CW > 0 && FCT > 0 && DP >= 8;
+}
+
+// The K^T operand (A of the dQ contraction, 16 dimensions x 32 keys in the
+// KS key order) of d-tile dt, read straight from the step's RT key tiles in
+// LDS with two transposing reads (ds_read_b64_tr_b16: within each 16-lane
+// group, lane i receives for r = 0..3 the 16-bit element i % 4 of the 8 bytes
+// that lane 4r + i / 4 of the group addresses).  Lane 16g + 4r + c addresses
+// key row 4g + r of key tile 0 (first read: k-slots 8g .. 8g+3 hold keys
+// 4g .. 4g+3) and of key tile 1 (second read: keys 16 + 4g .. +3), dimensions
+// 16 dt + 4c .. +3, through the XOR swizzle of the LDS columns.  The lane's
+// byte offsets within a chunk for even and odd dt (their 16-byte columns
+// differ by an XOR with 2) are computed once; everything else is an
+// immediate offset of the read.
+struct TrLane {
+  int even, odd;
+};
+__device__ __forceinline__ TrLane tr_lane(int lane) {
+  const int g = lane >> 4, r = (lane >> 2) & 3, c = lane & 3;
+  const int row = 4 * g + r;
+  const int col = (c >> 1) ^ ((row >> 1) & 3);
+  return {row * 64 + col * 16 + (c & 1) * 8, row * 64 + (col ^ 2) * 16 + (c & 1) * 8};
+}
+template <int DP>
+__device__ __forceinline__ uint4 kt_operand_tr(const char* kbase, int dt, TrLane t) {
+  typedef short short4v __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) short4v lds_short4v;
+  const char* p = kbase + ((dt & 1) ? t.odd : t.even) + (dt >> 1) * 1024;
+  const short4v a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p);
+  const short4v b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p + DP * 1024));
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  const u32x2 ua = __builtin_bit_cast(u32x2, a), ub = __builtin_bit_cast(u32x2, b);
+  return uint4{ua.x, ua.y, ub.x, ub.y};
+}
+
 // Rows of `width` floats starting at `base` can take 16-byte stores (every
 // row start 16-byte aligned).
 __device__ __forceinline__ bool vec4_rows(const float* base, int width) {
@@ -694,7 +736,17 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   constexpr int DT = 2 * DP;                // 16-row tiles of K^T (KS layout)
   constexpr int KCH = 2 * DP;               // chunks of K (RT) per step
   constexpr int VCH = 2 * CW;               // chunks of V (RT) per step
-  constexpr int TCH = DT;                   // chunks of K^T (KS) per step: 32 DP rows x 64 B
+  // The fused forward at D > 128 (several channels): qreg (64) and dQ (128
+  // registers) leave too few for the step's operands when all of a tile's
+  // score operands are held across the query tiles; in three phases with the
+  // operands read as they are used the pass fits in 256 registers without
+  // spills in the key loop (and the forward costs a few per cent of the pass
+  // instead of a pass of its own)
+  constexpr bool PHASED = CW > 0 && FCT > 0 && DP >= 8;
+  // K^T operands read from the RT key tiles by transposing LDS reads (no KS
+  // copy of the keys in the stream)
+  constexpr bool TR = dq_transposed_keys(std::is_same<T, F16>::value, DP, CW, FCT);
+  constexpr int TCH = TR ? 0 : DT;          // chunks of K^T (KS) per step: 32 DP rows x 64 B
   static_assert(!SV || CW == 0, "SVGD mode uses unit weights");
   constexpr int FCH = (CW > 0 || SV) ? FCT : 0;  // chunks of V^T (KS) per step, fused forward
   constexpr int NCH = KCH + VCH + TCH + FCH;
@@ -704,13 +756,6 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   constexpr bool WIDE = WPB == 2 * kWavesPerBlock;
   constexpr int NS = WIDE ? wide_stages(STAGE, NCH + 1) : ring_stages(STAGE, NCH + 1);
   constexpr int GW = CW > 0 ? CW : 1;       // RT chunks of the upstream gradient
-  // The fused forward at D > 128 (several channels): qreg (64) and dQ (128
-  // registers) leave too few for the step's operands when all of a tile's
-  // score operands are held across the query tiles; in three phases with the
-  // operands read as they are used the pass fits in 256 registers without
-  // spills in the key loop (and the forward costs a few per cent of the pass
-  // instead of a pass of its own)
-  constexpr bool PHASED = CW > 0 && FCH > 0 && DP >= 8;
   __shared__ __attribute__((aligned(1024))) char lds[NS * STAGE];
 
   const int lane = threadIdx.x & (kWave - 1);
@@ -838,6 +883,15 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
         b[qt] = pack_tile_pair(p);
       }
       __builtin_amdgcn_sched_barrier(0);
+      // the lane's transposing-read offsets, formed again in every step from
+      // the lane index (an opaque instruction pair, so the compiler cannot
+      // keep them live across the loop, where they would cost registers)
+      TrLane trl{0, 0};
+      if constexpr (TR) {
+        int ln;
+        asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+        trl = tr_lane(ln);
+      }
 #pragma unroll
       for (int ct = 0; ct < FCH; ++ct) {
         const uint4 a = fb[(16 * ct + j) * 4 + col];
@@ -846,12 +900,24 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
       }
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const uint4 a = tb[(16 * dt + j) * 4 + col];
+        const uint4 a = TR ? kt_operand_tr<DP>(base, dt, trl) : tb[(16 * dt + j) * 4 + col];
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
       }
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
+      if constexpr (TR) {
+        // keep each transposing read two d-tiles ahead of its MFMAs (the
+        // scheduler would otherwise issue all of them first and spill)
+        __builtin_amdgcn_sched_group_barrier(0x100, FCH + 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, FCH * QT, 0);
+#pragma unroll
+        for (int dt = 0; dt + 2 < DT; ++dt) {
+          __builtin_amdgcn_sched_group_barrier(0x008, QT, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * QT, 0);
+      }
       return;
     }
     uint4 ktr[DT];

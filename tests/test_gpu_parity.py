@@ -43,6 +43,10 @@ SHAPES = [
     (200, 333, 100, 32, "f16", "f32", "f16", None, 1.0),
     (300, 257, 128, 128, "f16", "f16", "f32", None, 1.0),
     (100, 150, 255, 3, "f16", "f32", "f32", None, 1.0),
+    # D > 128 with a fused forward-type sum: fp16 points take the K^T
+    # operands by transposing reads of the key tiles, bf16 points a KS copy
+    (90, 140, 200, 5, "bf16", "f32", "f32", None, 1.0),
+    (70, 530, 256, 16, "f16", "f16", "f32", None, 1.0),
     (96, 200, 256, 256, "f16", "f32", "f32", None, 1.0),
     (257, 97, 8, 64, "bf16", "f32", "f32", 0.5, 1.0),
     (33, 1000, 15, 1, "f16", "f32", "f32", None, 1.0),
