@@ -119,6 +119,16 @@ def kernel_sources_hash():
     return h.hexdigest()
 
 
+def dominant_kernel_name(workload):
+    """Name fragment of the kernel the roofline of `workload` is reported for
+    (the one whose traffic --traffic-from records)."""
+    if workload == "batch_grad_d32":
+        return "k_dq"
+    if workload.startswith("batch_"):
+        return "k_fwd32" if workload.endswith("_f32") else "k_fwd"
+    return "k_dq" if any(p != "fwd" for p in PASSES[workload]) else "k_fwd"
+
+
 def traffic_file(workload):
     return os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
 
@@ -315,6 +325,20 @@ def dominant_flops(passes, D, C, fused_call):
     return 2 * D + 2 * C
 
 
+def calibration_copy(mib, dev):
+    """Three device copies of `mib` MiB (the known-size kernel that --pmc runs
+    scale FETCH_SIZE / WRITE_SIZE by); nothing for mib = 0."""
+    if not mib:
+        return
+    import torch
+    src = torch.empty(mib * 1024 * 1024, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def clean(res):
     """The result without the private (underscore) entries."""
     return {k: v for k, v in res.items() if not k.startswith("_")}
@@ -394,14 +418,7 @@ def measure_workload(args, name, tau, steps, warmup, settle_ms, graph=False, flo
         if st != 0:
             raise gs.GaussSumError(st, "benchmark step")
 
-    if calibrate_copy:
-        nb = calibrate_copy * 1024 * 1024
-        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    calibration_copy(calibrate_copy, dev)
 
     settle_steps = 0
     t_settle = time.perf_counter()
@@ -613,6 +630,7 @@ def bench_batched(args):
     def step():
         gs.gauss_sum_fwd_batched(tq, tk, tv, float(tau), out=out, workspace=ws, stream=stream)
 
+    calibration_copy(args.calibrate_copy, dev)
     settle_steps, t0 = 0, time.perf_counter()
     while settle_steps == 0 or (time.perf_counter() - t0) * 1e3 < args.settle_ms:
         step()
@@ -709,6 +727,7 @@ def bench_batched_grad(args):
     def step():
         gs.gauss_sum_fwd_bwd_batched(tq, tk, tv, float(tau), tg, out=out, workspace=ws, stream=stream)
 
+    calibration_copy(args.calibrate_copy, dev)
     settle_steps, t0 = 0, time.perf_counter()
     while settle_steps == 0 or (time.perf_counter() - t0) * 1e3 < args.settle_ms:
         step()
@@ -754,7 +773,8 @@ def bench_batched_grad(args):
                      "achieved": grad_flops / (grad_ms * 1e-3) / 1e12, "peak": PEAK_MFMA_F16 / 1e12,
                      "unit": "TFLOP/s",
                      "frac": grad_flops / (grad_ms * 1e-3) / PEAK_MFMA_F16,
-                     "traffic": None, "avg_launch_ms": grad_ms / per_step, "launches": len(kernel_ms),
+                     "traffic": recorded_traffic(args.workload, "k_dq"),
+                     "avg_launch_ms": grad_ms / per_step, "launches": len(kernel_ms),
                      "launches_per_step": per_step, "flops_per_step": grad_flops,
                      "launch_share_of_step": grad_ms / ms_per_step},
     }
@@ -1141,9 +1161,8 @@ def main():
                          "gauss_sum_fwd_bwd call")
     args = ap.parse_args()
     if args.traffic_from:
-        grads_taken = any(p != "fwd" for p in PASSES[args.workload])
         traffic_from(args.workload, args.traffic_from[0], args.traffic_from[1],
-                     args.calibrate_copy * 1024 * 1024, "k_dq" if grads_taken else "k_fwd")
+                     args.calibrate_copy * 1024 * 1024, dominant_kernel_name(args.workload))
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
