@@ -95,8 +95,8 @@ typedef enum {
  * v_dtype: GS_F32, GS_F16 or GS_BF16. */
 typedef struct {
   int64_t M, N, D, C;
-  gs_dtype qk_dtype;
-  gs_dtype v_dtype;
+  int32_t qk_dtype; /* a gs_dtype value (an int field: any other value is rejected, not undefined) */
+  int32_t v_dtype;  /* a gs_dtype value */
 } gs_problem;
 
 /* Bytes of device workspace gauss_sum_fwd needs for problem p (0 if p is
@@ -140,7 +140,7 @@ gs_status gauss_sum_fwd_noalloc(const gs_problem* p, const void* q, const void* 
  * Any of dq, dk, dv may be NULL (not computed); at least one must be given.
  * Outputs are fp32 and overwritten. */
 gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
-                        const void* dout, gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                        const void* dout, int dout_dtype, float* dq, float* dk, float* dv,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Forward and backward in one call: writes out (as gauss_sum_fwd, required)
@@ -155,7 +155,7 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
  * Results equal those of separate gauss_sum_fwd and gauss_sum_bwd calls to
  * within the stated tolerance. */
 gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, const void* v,
-                            float tau, const void* dout, gs_dtype dout_dtype, float* out, float* dq,
+                            float tau, const void* dout, int dout_dtype, float* out, float* dq,
                             float* dk, float* dv, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
 
@@ -204,7 +204,7 @@ size_t gauss_sum_fwd_batched_workspace_size(const gs_problem* p, int64_t count);
  * slice is gauss_sum_bwd_workspace_size(p, ...) bytes). */
 gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
                                 const void* k, const void* v, float tau, const void* dout,
-                                gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                                int dout_dtype, float* dq, float* dk, float* dv,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Workspace bytes for gauss_sum_bwd_batched to run `count` problems in one
@@ -219,7 +219,7 @@ size_t gauss_sum_bwd_batched_workspace_size(const gs_problem* p, int64_t count, 
  * N sweep with B = 4 clouds). */
 gs_status gauss_sum_fwd_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
                                     const void* k, const void* v, float tau, const void* dout,
-                                    gs_dtype dout_dtype, float* out, float* dq, float* dk, float* dv,
+                                    int dout_dtype, float* out, float* dq, float* dk, float* dv,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Workspace bytes for gauss_sum_fwd_bwd_batched to run `count` problems in
@@ -270,8 +270,9 @@ gs_status gauss_sum_svgd(const gs_problem* p, const void* x, const void* score, 
  * update (M != N, C != D, invalid, or fp32 points) or N == 0. */
 size_t gauss_sum_svgd_workspace_size(const gs_problem* p);
 
-/* Static, never-NULL description of a status code. */
-const char* gauss_sum_status_string(gs_status s);
+/* Static, never-NULL description of a status code (any int: codes outside
+ * gs_status give "unknown status"). */
+const char* gauss_sum_status_string(int status);
 
 /* GAUSS_SUM_ABI_VERSION of the built library. */
 int gauss_sum_abi_version(void);

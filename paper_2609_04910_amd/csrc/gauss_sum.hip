@@ -653,7 +653,7 @@ inline dim3 grid_g(const Ctx& c, unsigned x, unsigned y = 1) { return dim3(x, y,
 // (as keys of a gradient pass) carries, and their stride; else NULL.
 template <typename T>
 void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t xs, int64_t n, int64_t n_pad, Side& s,
-                   uint32_t* slot, const void* sgn, gs_dtype sgn_dt, int64_t sgns) {
+                   uint32_t* slot, const void* sgn, int sgn_dt, int64_t sgns) {
   const gs_problem& p = *c.p;
   const int W = c.pl->dm.W();
   Bz bz = bz_ws(c);
@@ -679,7 +679,7 @@ void prep_points_t(const Ctx& c, const uint16_t* x16, int64_t xs, int64_t n, int
 }
 
 void prep_points(const Ctx& c, const void* x, int64_t xs, int64_t n, int64_t n_pad, Side& s,
-                 uint32_t* slot, const void* sgn = nullptr, gs_dtype sgn_dt = GS_F32, int64_t sgns = 0) {
+                 uint32_t* slot, const void* sgn = nullptr, int sgn_dt = GS_F32, int64_t sgns = 0) {
   const uint16_t* x16 = static_cast<const uint16_t*>(x);
   if (c.p->qk_dtype == GS_F16)
     prep_points_t<F16>(c, x16, xs, n, n_pad, s, slot, sgn, sgn_dt, sgns);
@@ -689,7 +689,7 @@ void prep_points(const Ctx& c, const void* x, int64_t xs, int64_t n, int64_t n_p
 
 // KS copy only (the second, differently signed copy of aliased points).
 void prep_points_ks(const Ctx& c, const void* x, int64_t xs, int64_t n, int64_t n_pad, uint16_t* ks,
-                    uint32_t* slot, const void* sgn, gs_dtype sgn_dt, int64_t sgns) {
+                    uint32_t* slot, const void* sgn, int sgn_dt, int64_t sgns) {
   const gs_problem& p = *c.p;
   const int W = c.pl->dm.W();
   const uint16_t* x16 = static_cast<const uint16_t*>(x);
@@ -705,7 +705,7 @@ void prep_points_ks(const Ctx& c, const void* x, int64_t xs, int64_t n, int64_t 
                        (int)p.D, n_pad, W, sl, sgn, (int)sgn_dt, ks, bz);
 }
 
-void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t xs, int64_t n, int64_t n_pad,
+void prep_values(const Ctx& c, const void* x, int dt, int64_t xs, int64_t n, int64_t n_pad,
                  Vals& s, uint32_t* slot) {
   const gs_problem& p = *c.p;
   const int Wv = c.pl->dm.Wv(), Rv = c.pl->dm.Rv();
@@ -725,7 +725,7 @@ void prep_values(const Ctx& c, const void* x, gs_dtype dt, int64_t xs, int64_t n
 // Per-step key scalars of key side `s` paired with values x (byte stride xs,
 // slot = their absolute maximum): single-channel problems fold log2|v| and
 // sign(v) in, otherwise half norms only.
-void prep_scalars(const Ctx& c, const Side& s, const void* x, gs_dtype dt, int64_t xs, int64_t n,
+void prep_scalars(const Ctx& c, const Side& s, const void* x, int dt, int64_t xs, int64_t n,
                   int64_t n_pad, const uint32_t* slot, float* out) {
   const bool vals = c.p->C == 1 && x != nullptr;
   Bz bz = bz_ws(c);
@@ -829,7 +829,7 @@ void pass_fwd(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t 
 // byte strides of out / out_s between problems.
 void pass_dq(const Ctx& c, const Side& qs, int64_t nq, const Side& ks, int64_t nk, const float* scal,
              const uint32_t* kslot, const uint16_t* vrt, const uint32_t* vslot, const uint16_t* grt,
-             const uint32_t* gslot, const void* g1, gs_dtype g1_dt, int64_t g1s, float* out, int64_t os,
+             const uint32_t* gslot, const void* g1, int g1_dt, int64_t g1s, float* out, int64_t os,
              const uint16_t* vks = nullptr, float* out_s = nullptr, int64_t os_s = 0) {
   const gs_problem& p = *c.p;
   const Dims& dm = c.pl->dm;
@@ -939,9 +939,9 @@ void fill_zero(hipStream_t st, float* p, int64_t n) {
 
 // ------------------------------------------------------------ validation
 
-size_t dsize(gs_dtype t) { return t == GS_F32 ? 4 : 2; }
+size_t dsize(int t) { return t == GS_F32 ? 4 : 2; }
 
-bool valid_dtype(gs_dtype t) { return t == GS_F32 || t == GS_F16 || t == GS_BF16; }
+bool valid_dtype(int t) { return t == GS_F32 || t == GS_F16 || t == GS_BF16; }
 
 gs_status check_problem(const gs_problem* p) {
   if (!p) return GS_ERR_NULL_POINTER;
@@ -1011,8 +1011,10 @@ extern "C" {
 int gauss_sum_abi_version(void) { return GAUSS_SUM_ABI_VERSION; }
 
 
-const char* gauss_sum_status_string(gs_status s) {
-  switch (s) {
+const char* gauss_sum_status_string(int status) {
+  // an int, not gs_status: a C caller may pass any code, and an enumeration
+  // object holding a value outside its range is undefined in C++
+  switch (status) {
     case GS_SUCCESS: return "success";
     case GS_ERR_NULL_POINTER: return "a required pointer is NULL or no output was requested";
     case GS_ERR_BAD_SHAPE: return "bad shape: need M, N >= 0 and 1 <= D, C <= 256";
@@ -1143,7 +1145,7 @@ int64_t group_size(const gs_problem& p, const Want& w, bool alias, int64_t cnt, 
 // sum, dq / dk / dv: gradients; NULL = not requested), each launch covering a
 // whole group on grid.z.
 gs_status run(const gs_problem* p, const gs_batch* b, const void* q, const void* k, const void* v,
-              float tau, const void* dout, gs_dtype dout_dtype, float* out, float* dq, float* dk,
+              float tau, const void* dout, int dout_dtype, float* out, float* dq, float* dk,
               float* dv, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   gs_status st = check_problem(p);
   if (st != GS_SUCCESS) return st;
@@ -1341,7 +1343,7 @@ gs_status gauss_sum_fwd(const gs_problem* p, const void* q, const void* k, const
 }
 
 gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const void* v, float tau,
-                        const void* dout, gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                        const void* dout, int dout_dtype, float* dq, float* dk, float* dv,
                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
     if (!dq && !dk && !dv) {
@@ -1358,7 +1360,7 @@ gs_status gauss_sum_bwd(const gs_problem* p, const void* q, const void* k, const
 }
 
 gs_status gauss_sum_fwd_bwd(const gs_problem* p, const void* q, const void* k, const void* v,
-                            float tau, const void* dout, gs_dtype dout_dtype, float* out, float* dq,
+                            float tau, const void* dout, int dout_dtype, float* out, float* dq,
                             float* dk, float* dv, void* workspace, size_t workspace_bytes,
                             hipStream_t stream) {
   try {
@@ -1576,7 +1578,7 @@ gs_status gauss_sum_fwd_batched(const gs_problem* p, const gs_batch* batch, cons
 
 gs_status gauss_sum_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
                                 const void* k, const void* v, float tau, const void* dout,
-                                gs_dtype dout_dtype, float* dq, float* dk, float* dv,
+                                int dout_dtype, float* dq, float* dk, float* dv,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
     if (!batch) {
@@ -1602,7 +1604,7 @@ size_t gauss_sum_fwd_bwd_batched_workspace_size(const gs_problem* p, int64_t cou
 }
 gs_status gauss_sum_fwd_bwd_batched(const gs_problem* p, const gs_batch* batch, const void* q,
                                     const void* k, const void* v, float tau, const void* dout,
-                                    gs_dtype dout_dtype, float* out, float* dq, float* dk, float* dv,
+                                    int dout_dtype, float* out, float* dq, float* dk, float* dv,
                                     void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
     if (!batch || (!out && batch->count > 0)) {
