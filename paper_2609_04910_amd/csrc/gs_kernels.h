@@ -545,45 +545,12 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
     }
   }
   const bool shifted = level == 1;
-  if (__syncthreads_or(level == 2)) {
-    // exact row maxima: the workgroup streams its key range once more through
-    // the LDS ring (keys and step scalars only); waves that need no offsets
-    // only take part in the copies and barriers
-    float smax[QT];
+  // level 2: the row maxima are tracked while streaming (running offset
+  // off = exponent of the largest value seen so far, -inf before the first
+  // step), instead of an exact pass over the keys first
+  if (level == 2) {
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) smax[qt] = -__builtin_inff();
-    auto issue_k = [&](int s, int stage) {
-      if (!mine) return;
-      const uint32_t base = lds0 + stage * STAGE;
-      const uint32_t ls = (uint32_t)(s - s_begin);
-#pragma unroll
-      for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, dlane);
-      dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
-    };
-    auto exact_compute = [&](int stage) {
-      if (level != 2) return;
-      const char* base = lds + stage * STAGE;
-      const uint4* kb = reinterpret_cast<const uint4*>(base);
-      const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        const floatx4 cin = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
-        uint4 kr[DP];
-        load_k_tile_lds<DP>(kb, kt, j, g, kr);
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) smax[qt] = max_into(smax[qt], score_tile<T, DP>(kr, qreg[qt], cin));
-      }
-    };
-    key_stream<NS, KCH + 1>(s_begin, s_end, issue_k, exact_compute);
-    __syncthreads();  // every wave is done with the ring before the main stream refills it
-    if (level == 2) {
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        off[qt] = fmaf(wave_max_over_g(smax[qt]), tau2, bq[qt]);
-        if (!(off[qt] > -__builtin_inff())) off[qt] = 0.0f;  // empty key range
-        bq[qt] -= off[qt];
-      }
-    }
+    for (int qt = 0; qt < QT; ++qt) off[qt] = -__builtin_inff();
   }
 
   settle(qreg);
@@ -596,8 +563,41 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
 
   // one key loop per range mode, so that each keeps the register budget of
   // a single loop body
-  auto compute = [&](int stage, auto shift_c) {
-    constexpr bool SH = decltype(shift_c)::value;
+  // Online offsets (level 2): before the exponentials of a query tile, the
+  // wave checks that no exponent y (relative to the current offset) exceeds
+  // kSigma; if one does, the offsets move up to the rows' largest exponent
+  // so far (exact, across the four key groups of each row) and the row's
+  // accumulators are rescaled by 2^(old - new).  Values are then at most
+  // 2^kSigma (fp16 holds them) and the largest of a row within 2^-kSigma of
+  // its maximum, as good as the exact offset for fp16 precision.  The check
+  // triggers only when a row's maximum grows by more than kSigma, a few
+  // times per row.
+  auto online_check = [&](int qt, const floatx4 (&a)[2]) {
+    float ymax = -__builtin_inff();
+    const float be = bq[qt] - off[qt];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ymax = fmaxf(ymax, fmaf(a[kt][r], tau2, be));
+    if (__any(ymax > kSigma)) {
+      float raw = -__builtin_inff();
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) raw = fmaxf(raw, fmaf(a[kt][r], tau2, bq[qt]));
+      const float nw = fmaxf(off[qt], wave_max_over_g(raw));
+      const float f = nw > off[qt] ? exp2f(off[qt] - nw) : 1.0f;
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) O[qt][ct][r] *= f;
+      off[qt] = nw;
+    }
+    return bq[qt] - off[qt];
+  };
+  auto compute = [&](int stage, auto mode_c) {
+    constexpr int MODE = decltype(mode_c)::value;
+    constexpr bool SH = MODE == 1;
     const char* base = lds + stage * STAGE;
     const uint4* kb = reinterpret_cast<const uint4*>(base);
     const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
@@ -612,7 +612,7 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
     const uint4* vb = reinterpret_cast<const uint4*>(base + KCH * 1024);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) vr[ct] = vb[(16 * ct + j) * 4 + lds_col(j, g)];
-    if constexpr (DP == 1 && CT == 1) {
+    if constexpr (DP == 1 && CT == 1 && MODE != 2) {
       // one 32-wide chunk and one value tile: all score MFMAs of the step,
       // then the exponentials, then the value contractions, kept apart by
       // scheduling barriers (3 % faster than tile by tile at D = 32 although
@@ -644,13 +644,24 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       float p[2][4];
+      if constexpr (MODE == 2) {
+        floatx4 acc[2];
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        const floatx4 acc = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
+        for (int kt = 0; kt < 2; ++kt) acc[kt] = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
+        const float be = online_check(qt, acc);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float y = fmaf(acc[r], tau2, bq[qt]);
-          p[kt][r] = SH ? exp2_shifted(y) : exp2_clamped(y);
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) p[kt][r] = __builtin_amdgcn_exp2f(fmaf(acc[kt][r], tau2, be));
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+          const floatx4 acc = score_tile<T, DP>(kr[kt], qreg[qt], cin[kt]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float y = fmaf(acc[r], tau2, bq[qt]);
+            p[kt][r] = SH ? exp2_shifted(y) : exp2_clamped(y);
+          }
         }
       }
       const uint4 b = pack_tile_pair(p);
@@ -658,10 +669,15 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
       for (int ct = 0; ct < CT; ++ct) O[qt][ct] = mfma_f16(vr[ct], b, O[qt][ct]);
     }
   };
-  if (shifted)
-    key_stream<NS, NCH + 1>(s_begin, s_end, issue, [&](int st) { compute(st, std::true_type{}); });
+  if (level == 2)
+    key_stream<NS, NCH + 1>(s_begin, s_end, issue,
+                            [&](int st) { compute(st, std::integral_constant<int, 2>{}); });
+  else if (shifted)
+    key_stream<NS, NCH + 1>(s_begin, s_end, issue,
+                            [&](int st) { compute(st, std::integral_constant<int, 1>{}); });
   else
-    key_stream<NS, NCH + 1>(s_begin, s_end, issue, [&](int st) { compute(st, std::false_type{}); });
+    key_stream<NS, NCH + 1>(s_begin, s_end, issue,
+                            [&](int st) { compute(st, std::integral_constant<int, 0>{}); });
 
   const int ev = scale_exponent(*vslot) - (ONE ? 1 : 0);
   const bool v4 = vec4_rows(out, C);
