@@ -66,7 +66,7 @@ def check_problem(label, b, q, k, v, g, tau, out, dq=None, dk=None, dv=None):
 SHAPES = [(4, 300, 517, 32, 1), (3, 64, 1000, 64, 3), (5, 129, 97, 17, 2), (6, 700, 640, 16, 1)]
 
 
-@pytest.mark.parametrize("B,M,N,D,C", SHAPES)
+@pytest.mark.parametrize("B,M,N,D,C", SHAPES + [(2, 100, 300, 256, 5)])
 def test_batched_matches_oracle_every_problem(B, M, N, D, C):
     import torch
     from paper_2609_04910_amd import gauss_sum as gs
@@ -106,7 +106,7 @@ def test_one_slice_workspace_equals_single_calls(B, M, N, D, C):
             assert torch.equal(x[b], y)
 
 
-@pytest.mark.parametrize("B,M,N,D,C", [SHAPES[0], SHAPES[1], (4, 257, 1500, 32, 1)])
+@pytest.mark.parametrize("B,M,N,D,C", [SHAPES[0], SHAPES[1], (4, 257, 1500, 32, 1), (3, 130, 700, 256, 16)])
 def test_fwd_bwd_batched(B, M, N, D, C):
     """gauss_sum_fwd_bwd_batched: every problem against the oracle (all four
     outputs, one launch group), bitwise equal to the single-problem

@@ -21,7 +21,7 @@ def _setup(M, N, D, C, seed):
 
 
 @pytest.mark.parametrize("M,N,D,C,mode", [(4096, 4096, 16, 1, "fwd"), (3000, 5000, 64, 1, "fwd_bwd"),
-                                          (1000, 1500, 40, 12, "fwd_bwd")])
+                                          (1000, 1500, 40, 12, "fwd_bwd"), (700, 1200, 256, 16, "fwd_bwd")])
 def test_graph_replays_match_eager(M, N, D, C, mode):
     import torch
     from paper_2609_04910_amd import gauss_sum as gs
