@@ -535,8 +535,8 @@ void make_plan(const gs_problem& p, const Want& w, bool alias, void* ws, Plan& p
   // its K^T operands from the RT tiles (dq_transposed_keys)
   const bool f16 = p.qk_dtype == GS_F16;
   const int cw = dq_cw(p, pl.dm);
-  const bool need_k_ks = w.dq && !dq_transposed_keys(f16, pl.dm.DP, cw, w.fused() ? 1 : 0);
-  const bool need_q_ks = w.dk && !dq_transposed_keys(f16, pl.dm.DP, cw, w.fused_kv() ? 1 : 0);
+  const bool need_k_ks = w.dq && !dq_transposed_keys(f16, pl.dm.DP, cw);
+  const bool need_q_ks = w.dk && !dq_transposed_keys(f16, pl.dm.DP, cw);
   // sample of a key side: its half norms are followed by the row-bound flags
   // of the rows queried against it (the other side's padded row count)
   auto side = [&](Side& s, int64_t n_pad, bool ks, bool sample, int64_t other_pad) {

@@ -397,14 +397,22 @@ __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
   return b;
 }
 
+// Whether the gradient kernel runs a step in three phases (all score MFMAs,
+// then the w contractions and exponentials, then the contractions over keys,
+// each LDS operand read as it is used): several channels at D > 64 where the
+// pass then fits in 256 registers without spills in the key loop (checked
+// per instance: D <= 128 with C <= 128, D <= 256 with C <= 32 or C > 224).
+constexpr bool dq_phased(int DP, int CW) {
+  return CW > 0 && ((DP == 4 && CW <= 4) || (DP == 8 && (CW == 1 || CW == 8)));
+}
+
 // Whether the gradient kernel takes its K^T operands from the streamed RT
 // key tiles by transposing LDS reads instead of streaming a KS copy of the
 // keys: fp16 points only (the RT tiles then hold exactly the fp16 values the
-// contraction needs; a bf16 KS copy is converted to fp16), and only for the
-// three-phase step (several channels with a fused forward-type sum, D > 128).
-// The host planner uses the same rule to leave out the KS copy.
-constexpr bool dq_transposed_keys(bool f16_points, int DP, int CW, int FCT) {
-  return f16_points && CW > 0 && FCT > 0 && DP >= 8;
+// contraction needs; a bf16 KS copy is converted to fp16), in the three-phase
+// step.  The host planner uses the same rule to leave out the KS copy.
+constexpr bool dq_transposed_keys(bool f16_points, int DP, int CW) {
+  return f16_points && dq_phased(DP, CW);
 }
 
 // The K^T operand (A of the dQ contraction, 16 dimensions x 32 keys in the
@@ -752,16 +760,15 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   constexpr int DT = 2 * DP;                // 16-row tiles of K^T (KS layout)
   constexpr int KCH = 2 * DP;               // chunks of K (RT) per step
   constexpr int VCH = 2 * CW;               // chunks of V (RT) per step
-  // The fused forward at D > 128 (several channels): qreg (64) and dQ (128
-  // registers) leave too few for the step's operands when all of a tile's
-  // score operands are held across the query tiles; in three phases with the
-  // operands read as they are used the pass fits in 256 registers without
-  // spills in the key loop (and the forward costs a few per cent of the pass
-  // instead of a pass of its own)
-  constexpr bool PHASED = CW > 0 && FCT > 0 && DP >= 8;
+  // At D = 256 qreg (64) and dQ (128 registers) leave too few for the step's
+  // operands when all of a tile's score operands are held across the query
+  // tiles; in three phases with the operands read as they are used the pass
+  // fits (and the fused forward costs a few per cent of the pass instead of
+  // a pass of its own)
+  constexpr bool PHASED = dq_phased(DP, CW);
   // K^T operands read from the RT key tiles by transposing LDS reads (no KS
   // copy of the keys in the stream)
-  constexpr bool TR = dq_transposed_keys(std::is_same<T, F16>::value, DP, CW, FCT);
+  constexpr bool TR = dq_transposed_keys(std::is_same<T, F16>::value, DP, CW);
   constexpr int TCH = TR ? 0 : DT;          // chunks of K^T (KS) per step: 32 DP rows x 64 B
   static_assert(!SV || CW == 0, "SVGD mode uses unit weights");
   constexpr int FCH = (CW > 0 || SV) ? FCT : 0;  // chunks of V^T (KS) per step, fused forward
