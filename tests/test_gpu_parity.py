@@ -253,6 +253,34 @@ def test_range_levels_plain_shifted_exact():
     _say("  stats", parity.check_workload(w))
 
 
+@pytest.mark.parametrize("D", [32, 128])
+def test_online_offsets_rescale(D):
+    """Rows far below their sampled maxima (the forward's running row
+    maximum) with the keys in order of decreasing distance from the queries:
+    the largest kernel value of a row grows from about 2^-400 in the first
+    key steps to about 2^-30 in the last, so the running offsets are raised
+    (and the accumulators rescaled) many times on the way; the forward
+    matches the oracle."""
+    import parity
+    rng = np.random.default_rng(17 + D)
+    M, N, C = 700, 4000, 4
+    tau = np.float32(1.0)
+    c = float(tau) * np.log2(np.e) / 2.0
+    centre = rng.standard_normal(D)
+    q = centre + 0.05 * rng.standard_normal((M, D))
+    u = rng.standard_normal((N, D))
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    r = np.sqrt(np.linspace(400.0, 30.0, N) / c)   # -log2 Phi from 400 down to 30
+    k = centre + u * r[:, None]
+    q16, k16 = q.astype(np.float16), k.astype(np.float16)
+    d2 = ((q16.astype(np.float64)[:, None, :] - k16.astype(np.float64)[None, :, :]) ** 2).sum(-1)
+    L = -c * d2
+    assert np.all(L.max(axis=1) < -23) and np.all(L[:, :200].max(axis=1) < L.max(axis=1) - 60)
+    v = rng.standard_normal((N, C)).astype(np.float32)
+    w = wl.Workload("online_rescale", M, N, D, C, tau, "f16", q16, k16, v, None, ("fwd",), False, q16, k16)
+    _say("  stats", parity.check_workload(w, passes=("fwd",)))
+
+
 def test_many_keys_split_limit():
     """2^23 + 100 keys at D = 256 with enough query rows that one key split
     would fill the GPU: the planner must still split the keys so that no
