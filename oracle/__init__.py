@@ -45,6 +45,10 @@ def load(path):
         args += [ctypes.c_double, ip, i64, dp, dp, ctypes.c_int]
         fn.argtypes = args
         fn.restype = ctypes.c_int
+    for name in ("gs_oracle_dq_scales", "gs_oracle_dk_scales"):
+        fn = getattr(lib, name)
+        fn.argtypes = [i64, i64, i64, i64, dp, dp, dp, dp, ctypes.c_double, ip, i64, dp, dp, dp, ctypes.c_int]
+        fn.restype = ctypes.c_int
     return lib
 
 
@@ -83,7 +87,7 @@ def _rows(rows, limit):
     return r, r.size
 
 
-def _call(lib, name, q, k, v, g, tau, rows, out_width_is_c, key_rows, threads):
+def _call(lib, name, q, k, v, g, tau, rows, out_width_is_c, key_rows, threads, net=False):
     q, k, v = _f64(q), _f64(k), _f64(v)
     M, D = q.shape
     N, Dk = k.shape
@@ -98,17 +102,21 @@ def _call(lib, name, q, k, v, g, tau, rows, out_width_is_c, key_rows, threads):
     width = C if out_width_is_c else D
     out = np.zeros((nrows, width), dtype=np.float64)
     absout = np.zeros((nrows, width), dtype=np.float64)
+    netout = np.zeros((nrows, width), dtype=np.float64) if net else None
     rp = r.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if r is not None else None
     fn = getattr(lib, name)
     nt = threads or default_threads()
     args = [M, N, D, C, _ptr(q), _ptr(k), _ptr(v)]
     if g is not None:
         args.append(_ptr(g))
-    args += [float(tau), rp, nrows, _ptr(out), _ptr(absout), nt]
+    args += [float(tau), rp, nrows, _ptr(out), _ptr(absout)]
+    if net:
+        args.append(_ptr(netout))
+    args.append(nt)
     st = fn(*args)
     if st != 0:
         raise ValueError("%s failed with status %d" % (name, st))
-    return out, absout
+    return (out, absout, netout) if net else (out, absout)
 
 
 class Oracle:
@@ -133,6 +141,15 @@ class Oracle:
         """dL/dk on key rows ``rows``: returns (dk, scale)."""
         return _call(self.lib, "gs_oracle_dk", q, k, v, g, tau, rows, False, True, threads)
 
+    def dq_scales(self, q, k, v, g, tau, rows=None, threads=None):
+        """dq with both scales: returns (dq, sum of |terms| over (n, c),
+        tau sum_n Phi |w_mn| |k_n - q_m| (net over c))."""
+        return _call(self.lib, "gs_oracle_dq_scales", q, k, v, g, tau, rows, False, False, threads, net=True)
+
+    def dk_scales(self, q, k, v, g, tau, rows=None, threads=None):
+        """dk with both scales, as dq_scales."""
+        return _call(self.lib, "gs_oracle_dk_scales", q, k, v, g, tau, rows, False, True, threads, net=True)
+
     def dv(self, q, k, v, g, tau, rows=None, threads=None):
         """dL/dv on key rows ``rows``: returns (dv, scale)."""
         return _call(self.lib, "gs_oracle_dv", q, k, v, g, tau, rows, True, True, threads)
@@ -143,3 +160,5 @@ fwd = _DEFAULT.fwd
 dq = _DEFAULT.dq
 dk = _DEFAULT.dk
 dv = _DEFAULT.dv
+dq_scales = _DEFAULT.dq_scales
+dk_scales = _DEFAULT.dk_scales

@@ -27,7 +27,10 @@
  * absolute values of its terms, the scale against which a reduced-precision
  * result is judged: A = sum_n Phi |v_n| for the sum, and for the q and k
  * gradients, which are double sums over (n, c) of tau Phi g_c v_c (k - q),
- * tau sum Phi (sum_c |g_c v_c|) |k - q|.
+ * tau sum Phi (sum_c |g_c v_c|) |k - q|.  The *_scales variants of the q and k
+ * gradients also return the net scale tau sum Phi |sum_c g_c v_c| |k - q|, in
+ * which the C terms of each w are summed before the magnitude is taken (the
+ * other reading of the gradient tolerance, at most the first).
  *
  * Parallelism: output rows are independent; rows are split into contiguous
  * chunks over POSIX threads.  Each row is summed by one thread in index
@@ -54,6 +57,7 @@ typedef struct {
   const int64_t* rows; /* selected output rows, or NULL for 0..nrows-1 */
   int64_t row_begin, row_end;
   double *out, *absout;
+  double* netout; /* q / k gradients: tau sum Phi |w| |k - q|, or NULL */
 } job_t;
 
 /* Phi(a, b) = exp(-tau/2 * sum_d (a_d - b_d)^2): Eq. 1, difference form. */
@@ -98,10 +102,10 @@ static void fwd_row(const job_t* j, int64_t m, double* o, double* a) {
  * values contracted against g_m).  As a double sum over (n, c) its terms are
  * tau Phi g_mc v_nc (k_n - q_m), so the scale is
  * Aq = tau sum_n Phi (sum_c |g_mc v_nc|) |k_n - q_m|. */
-static void dq_row(const job_t* j, int64_t m, double* o, double* a) {
+static void dq_row(const job_t* j, int64_t m, double* o, double* a, double* nt) {
   const double* qm = j->q + m * j->D;
   const double* gm = j->g + m * j->C;
-  for (int64_t d = 0; d < j->D; ++d) { o[d] = 0.0; a[d] = 0.0; }
+  for (int64_t d = 0; d < j->D; ++d) { o[d] = 0.0; a[d] = 0.0; if (nt) nt[d] = 0.0; }
   for (int64_t n = 0; n < j->N; ++n) {
     const double* kn = j->k + n * j->D;
     double p = phi(qm, kn, j->D, j->tau);
@@ -111,16 +115,17 @@ static void dq_row(const job_t* j, int64_t m, double* o, double* a) {
       double diff = kn[d] - qm[d];
       o[d] += j->tau * p * w * diff;
       a[d] += j->tau * p * wa * fabs(diff);
+      if (nt) nt[d] += j->tau * p * fabs(w) * fabs(diff);
     }
   }
 }
 
 /* dk_n = tau sum_m Phi w (q_m - k_n) and its scale
  * Ak = tau sum_m Phi (sum_c |g_mc v_nc|) |q_m - k_n|. */
-static void dk_row(const job_t* j, int64_t n, double* o, double* a) {
+static void dk_row(const job_t* j, int64_t n, double* o, double* a, double* nt) {
   const double* kn = j->k + n * j->D;
   const double* vn = j->v + n * j->C;
-  for (int64_t d = 0; d < j->D; ++d) { o[d] = 0.0; a[d] = 0.0; }
+  for (int64_t d = 0; d < j->D; ++d) { o[d] = 0.0; a[d] = 0.0; if (nt) nt[d] = 0.0; }
   for (int64_t m = 0; m < j->M; ++m) {
     const double* qm = j->q + m * j->D;
     double p = phi(qm, kn, j->D, j->tau);
@@ -130,6 +135,7 @@ static void dk_row(const job_t* j, int64_t n, double* o, double* a) {
       double diff = qm[d] - kn[d];
       o[d] += j->tau * p * w * diff;
       a[d] += j->tau * p * wa * fabs(diff);
+      if (nt) nt[d] += j->tau * p * fabs(w) * fabs(diff);
     }
   }
 }
@@ -155,10 +161,11 @@ static void* run_job(void* arg) {
     int64_t row = j->rows ? j->rows[r] : r;
     double* o = j->out + r * width;
     double* a = j->absout + r * width;
+    double* nt = j->netout ? j->netout + r * width : NULL;
     switch (j->op) {
       case OP_FWD: fwd_row(j, row, o, a); break;
-      case OP_DQ: dq_row(j, row, o, a); break;
-      case OP_DK: dk_row(j, row, o, a); break;
+      case OP_DQ: dq_row(j, row, o, a, nt); break;
+      case OP_DK: dk_row(j, row, o, a, nt); break;
       default: dv_row(j, row, o, a); break;
     }
   }
@@ -204,7 +211,7 @@ static int dispatch(job_t base, int64_t nrows, int nthreads) {
 int gs_oracle_fwd(int64_t M, int64_t N, int64_t D, int64_t C, const double* q, const double* k,
                   const double* v, double tau, const int64_t* rows, int64_t nrows, double* out,
                   double* absout, int nthreads) {
-  job_t j = {OP_FWD, M, N, D, C, q, k, v, NULL, tau, rows, 0, 0, out, absout};
+  job_t j = {OP_FWD, M, N, D, C, q, k, v, NULL, tau, rows, 0, 0, out, absout, NULL};
   return dispatch(j, nrows, nthreads);
 }
 
@@ -213,7 +220,7 @@ int gs_oracle_fwd(int64_t M, int64_t N, int64_t D, int64_t C, const double* q, c
 int gs_oracle_dq(int64_t M, int64_t N, int64_t D, int64_t C, const double* q, const double* k,
                  const double* v, const double* g, double tau, const int64_t* rows, int64_t nrows,
                  double* out, double* absout, int nthreads) {
-  job_t j = {OP_DQ, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout};
+  job_t j = {OP_DQ, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout, NULL};
   return dispatch(j, nrows, nthreads);
 }
 
@@ -221,7 +228,28 @@ int gs_oracle_dq(int64_t M, int64_t N, int64_t D, int64_t C, const double* q, co
 int gs_oracle_dk(int64_t M, int64_t N, int64_t D, int64_t C, const double* q, const double* k,
                  const double* v, const double* g, double tau, const int64_t* rows, int64_t nrows,
                  double* out, double* absout, int nthreads) {
-  job_t j = {OP_DK, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout};
+  job_t j = {OP_DK, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout, NULL};
+  return dispatch(j, nrows, nthreads);
+}
+
+/* gs_oracle_dq, also writing the net scale tau sum_n Phi |w| |k_n - q_m| to
+ * netout (nrows x D). */
+int gs_oracle_dq_scales(int64_t M, int64_t N, int64_t D, int64_t C, const double* q,
+                        const double* k, const double* v, const double* g, double tau,
+                        const int64_t* rows, int64_t nrows, double* out, double* absout,
+                        double* netout, int nthreads) {
+  job_t j = {OP_DQ, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout, netout};
+  if (nrows && !netout) return 1;
+  return dispatch(j, nrows, nthreads);
+}
+
+/* gs_oracle_dk, also writing the net scale tau sum_m Phi |w| |q_m - k_n|. */
+int gs_oracle_dk_scales(int64_t M, int64_t N, int64_t D, int64_t C, const double* q,
+                        const double* k, const double* v, const double* g, double tau,
+                        const int64_t* rows, int64_t nrows, double* out, double* absout,
+                        double* netout, int nthreads) {
+  job_t j = {OP_DK, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout, netout};
+  if (nrows && !netout) return 1;
   return dispatch(j, nrows, nthreads);
 }
 
@@ -229,6 +257,6 @@ int gs_oracle_dk(int64_t M, int64_t N, int64_t D, int64_t C, const double* q, co
 int gs_oracle_dv(int64_t M, int64_t N, int64_t D, int64_t C, const double* q, const double* k,
                  const double* v, const double* g, double tau, const int64_t* rows, int64_t nrows,
                  double* out, double* absout, int nthreads) {
-  job_t j = {OP_DV, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout};
+  job_t j = {OP_DV, M, N, D, C, q, k, v, g, tau, rows, 0, 0, out, absout, NULL};
   return dispatch(j, nrows, nthreads);
 }

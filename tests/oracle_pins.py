@@ -317,6 +317,43 @@ def pin_gradient_scales(orc):
     _close(orc.dv(q, k, v, g, tau)[1], av, 1e-12, 1e-300, "dv scale")
 
 
+def pin_net_scales(orc):
+    """The net scales tau sum Phi |sum_c g_c v_c| |k - q| of the q and k
+    gradients: from the dense kernel matrix; equal to the absolute scales for
+    one channel; zero where every w_mn vanishes although its channel terms do
+    not (g_m = (a, a), v_n = (b, -b)), unlike the absolute scale; never above the absolute
+    scale; and the gradients themselves unchanged."""
+    q, k, v, g = _problem(31, 6, 8, 3, 3)
+    tau = 0.7
+    Kmat = _kernel_matrix(q, k, tau).astype(np.float64)
+    Wn = np.abs(g @ v.T)                           # |sum_c g_mc v_nc|
+    diff = k[None, :, :] - q[:, None, :]
+    nq = tau * np.einsum("mn,mnd->md", Kmat * Wn, np.abs(diff))
+    nk = tau * np.einsum("mn,mnd->nd", Kmat * Wn, np.abs(diff))
+    dq, aq, netq = orc.dq_scales(q, k, v, g, tau)
+    dk, ak, netk = orc.dk_scales(q, k, v, g, tau)
+    _close(netq, nq, 1e-12, 1e-300, "dq net scale")
+    _close(netk, nk, 1e-12, 1e-300, "dk net scale")
+    assert np.all(netq <= aq * (1 + 1e-12)) and np.all(netk <= ak * (1 + 1e-12))
+    _close(dq, orc.dq(q, k, v, g, tau)[0], 0.0, 0.0, "dq value")
+    _close(dk, orc.dk(q, k, v, g, tau)[0], 0.0, 0.0, "dk value")
+    # one channel: |g v| = |g| |v|, the two scales agree
+    q1, k1, v1, g1 = _problem(32, 5, 7, 2, 1)
+    _, a1, n1 = orc.dq_scales(q1, k1, v1, g1, 0.9)
+    _close(n1, a1, 1e-14, 0.0, "one-channel dq scales")
+    _, a1k, n1k = orc.dk_scales(q1, k1, v1, g1, 0.9)
+    _close(n1k, a1k, 1e-14, 0.0, "one-channel dk scales")
+    # w = a_m b_n - a_m b_n = 0 for every pair while each channel's term is not
+    a = _rng(33).standard_normal((6, 1))
+    b = _rng(34).standard_normal((8, 1))
+    g2 = np.hstack([a, a])
+    v2 = np.hstack([b, -b])
+    d2, a2, n2 = orc.dq_scales(q, k, v2, g2, tau)
+    assert np.all(n2 == 0.0) and np.all(d2 == 0.0) and np.all(a2 > 0.0)
+    d2k, a2k, n2k = orc.dk_scales(q, k, v2, g2, tau)
+    assert np.all(n2k == 0.0) and np.all(d2k == 0.0) and np.all(a2k > 0.0)
+
+
 def pin_swap_identities(orc):
     """Eq. 1 is symmetric in (q, k) and linear in v, so
     dv(q,k,v,g) = s(k,q,g) and dk(q,k,v,g) = dq(k,q,g,v)."""

@@ -69,8 +69,31 @@ def oracle_ref(w, pas, rows=None, g=None):
     th = oracle_threads()
     if pas == "fwd":
         return oracle.fwd(qv, kv, w.v, float(w.tau), rows=rows, threads=th)
-    fn = {"dq": oracle.dq, "dk": oracle.dk, "dv": oracle.dv}[pas]
+    if pas in ("dq", "dk"):
+        # value and absolute scale; the net scale (w summed over channels
+        # before the magnitude) is kept for net_ratio
+        fn = oracle.dq_scales if pas == "dq" else oracle.dk_scales
+        val, absscale, net = fn(qv, kv, w.v, g, float(w.tau), rows=rows, threads=th)
+        NET_SCALES[id(val)] = net
+        return val, absscale
+    fn = {"dv": oracle.dv}[pas]
     return fn(qv, kv, w.v, g, float(w.tau), rows=rows, threads=th)
+
+
+# net scales of the gradient references oracle_ref returned, by id of the value array
+NET_SCALES = {}
+
+
+def net_ratio(got, ref):
+    """max |gpu - oracle| / net scale over the elements whose net scale is at
+    least 1e-3 of the row's largest (the other reading of the gradient
+    tolerance; elements whose w cancel almost completely are left out)."""
+    net = NET_SCALES.get(id(ref))
+    if net is None or not net.size:
+        return None
+    err = np.abs(np.asarray(got, dtype=np.float64) - ref)
+    keep = net >= 1e-3 * np.max(net, axis=1, keepdims=True)
+    return float(np.max(np.where(keep, err / np.maximum(net, 1e-300), 0.0)))
 
 
 def compare(label, got, ref, scale, tol):
@@ -114,6 +137,10 @@ def check_workload(w, passes=None, rows=None, key_rows=None, alias=True, label=N
             g = got[p] if r is None else got[p][np.asarray(r)]
             key = p + ("/fused" if f else "")
             stats[key] = compare("%s/%s" % (label, key), g, ref, scale, tol)
+            nr = net_ratio(g, ref)
+            if nr is not None:
+                stats[key + "/net"] = nr
+    NET_SCALES.clear()
     if len(results) == 2:
         sep, fus = results[0][1], results[1][1]
         for p in ("dk", "dv"):

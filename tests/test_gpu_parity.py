@@ -176,6 +176,21 @@ REDUCED = {
 }
 
 
+def _check_net(name, tau, stats, qk_dtype):
+    """The gradients also meet the tolerance against the net scale
+    tau sum Phi |sum_c g_c v_c| |k - q| (w summed over the channels before the
+    magnitude) on the benchmark workloads; mixture_d32 at tau = 10, whose rows
+    are dominated by a few keys, is the exception (there a nearly cancelling
+    w of the dominant pair meets the fp16 rounding of g and v: 1.2e-2 and
+    4.8e-2 for dq and dk, against 7e-4 of the absolute scale)."""
+    import parity
+    if name == "mixture_d32" and tau == 10.0:
+        return
+    for key, val in stats.items():
+        if key.endswith("/net"):
+            assert val <= parity.TOL[qk_dtype], (name, key, val)
+
+
 @pytest.mark.parametrize("name", wl.ORDER)
 def test_workload_reduced_size_all_rows(name):
     import parity
@@ -185,6 +200,7 @@ def test_workload_reduced_size_all_rows(name):
         _say("workload", name, "tau", w.tau, "M", w.M, "N", w.N)
         stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
         _say("  stats", stats)
+        _check_net(name, tau, stats, w.qk_dtype)
 
 
 # Sampled query rows / key rows per workload, sized so the oracle checks each
@@ -210,6 +226,7 @@ def test_workload_full_size_sampled_rows(name):
         _say("workload", name, "tau", w.tau, "full size", w.M, w.N)
         stats = parity.check_workload(w, rows=rows, key_rows=key_rows)
         _say("  stats", stats)
+        _check_net(name, tau, stats, w.qk_dtype)
         if name == "rect_d256":
             # the query gradient on 1024 sampled rows (each against all 2^21 keys)
             rows = wl.sample_rows(w.M, 1024, seed=3)

@@ -19,8 +19,10 @@ MUTANTS = [
     ("fwd_wrong_value_row", "const double* vn = j->v + n * j->C;\n    double p = phi(qm", "const double* vn = j->v + (n % 2) * j->C;\n    double p = phi(qm"),
     ("abs_scale_not_abs", "a[c] += p * fabs(vn[c]);", "a[c] += p * vn[c];"),
     ("dq_sign", "double diff = kn[d] - qm[d];", "double diff = qm[d] - kn[d];"),
-    ("dq_no_tau", "o[d] += j->tau * p * w * diff;\n      a[d] += j->tau * p * wa * fabs(diff);\n    }\n  }\n}\n\n/* dk_n",
-     "o[d] += p * w * diff;\n      a[d] += j->tau * p * wa * fabs(diff);\n    }\n  }\n}\n\n/* dk_n"),
+    ("dq_no_tau", "o[d] += j->tau * p * w * diff;\n      a[d] += j->tau * p * wa * fabs(diff);\n      if (nt) nt[d] += j->tau * p * fabs(w) * fabs(diff);\n    }\n  }\n}\n\n/* dk_n",
+     "o[d] += p * w * diff;\n      a[d] += j->tau * p * wa * fabs(diff);\n      if (nt) nt[d] += j->tau * p * fabs(w) * fabs(diff);\n    }\n  }\n}\n\n/* dk_n"),
+    ("net_scale_no_abs", "if (nt) nt[d] += j->tau * p * fabs(w) * fabs(diff);", "if (nt) nt[d] += j->tau * p * w * fabs(diff);"),
+    ("net_scale_uses_abs_terms", "if (nt) nt[d] += j->tau * p * fabs(w) * fabs(diff);", "if (nt) nt[d] += j->tau * p * wa * fabs(diff);"),
     ("grad_scale_uses_w", "a[d] += j->tau * p * wa * fabs(diff);", "a[d] += j->tau * p * fabs(w) * fabs(diff);"),
     ("dq_transposed_g", "const double* gm = j->g + m * j->C;\n  for (int64_t d", "const double* gm = j->g + (m % 2) * j->C;\n  for (int64_t d"),
     ("dk_sign", "double diff = qm[d] - kn[d];", "double diff = kn[d] - qm[d];"),
