@@ -16,6 +16,9 @@ Each call returns ``(value, scale)`` where ``scale`` is the sum of absolute
 values of the terms, the yardstick for the tolerance of a reduced-precision
 evaluation: sum_n Phi |v_n| for the sum and dv, and for dq / dk (double sums
 over keys and channels) tau sum_n Phi (sum_c |g_c v_c|) |k_n - q_m|.
+``dq_scales`` / ``dk_scales`` also return the net scale
+tau sum_n Phi |sum_c g_c v_c| |k_n - q_m| (the channels summed before the
+magnitude: the other reading of the gradient tolerance, at most the first).
 
 Inputs are converted to fp64 from whatever dtype they hold (float16, float32,
 float64; bf16 must be passed already upcast), so the oracle sees exactly the
