@@ -506,6 +506,8 @@ def measure_workload(args, name, tau, steps, warmup, settle_ms, graph=False, flo
         "warmup": warmup,
         "settle": {"ms": settle_ms_done, "steps": settle_steps},
         "ms_per_step": ms_per_step,
+        # device memory beyond inputs and outputs (the caller-owned workspace)
+        "workspace_bytes": int(ws.numel()),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -561,7 +563,8 @@ def sub_record(res, tau=None):
            "ms_per_step": res["ms_per_step"], "pairs_per_s": res["value"],
            "step_frac_of_mfma_peak": res["step_roofline"]["frac"],
            "kernel": res["roofline"]["kernel"], "avg_launch_ms": res["roofline"]["avg_launch_ms"],
-           "kernel_frac_of_mfma_peak": res["roofline"]["frac"]}
+           "kernel_frac_of_mfma_peak": res["roofline"]["frac"],
+           "workspace_bytes": res.get("workspace_bytes")}
     if c["D"] <= 32:
         # one exponential per pair and pass: the target for D <= 32 is stated
         # against the exponential rate
