@@ -447,6 +447,46 @@ __device__ __forceinline__ uint4 kt_operand_tr(const char* kbase, int dt, TrLane
   return uint4{ua.x, ua.y, ub.x, ub.y};
 }
 
+// LDS reads issued as assembly with immediate offsets, for operands that are
+// read well ahead of their use: the compiler neither sinks such a read to its
+// first use nor counts it in its own waits, so the reader waits explicitly
+// (lgkm_fence) before that use.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <int OFF>
+__device__ __forceinline__ u32x2 ds_read_tr_b64_asm(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+  return r;
+}
+template <int OFF>
+__device__ __forceinline__ u32x4 ds_read_b128_asm(uint32_t addr) {
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+  return r;
+}
+// Wait until at most N LDS operations of the wave are outstanding (LDS reads
+// complete in order, so every read issued before the N newest is done).  The
+// operands pass through the statement, so their uses cannot move above it.
+template <int N>
+__device__ __forceinline__ void lgkm_fence(u32x2& a, u32x2& b) {
+  asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a), "+v"(b) : "n"(N));
+}
+template <int N>
+__device__ __forceinline__ void lgkm_fence(u32x4& a) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(a) : "n"(N));
+}
+
+// f(integral_constant<int, I>) for I = B .. E-1, for code whose immediates
+// depend on the index.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 // Rows of `width` floats starting at `base` can take 16-byte stores (every
 // row start 16-byte aligned).
 __device__ __forceinline__ bool vec4_rows(const float* base, int width) {
@@ -914,6 +954,44 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
         int ln;
         asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
         trl = tr_lane(ln);
+        // the V^T tiles, then the K^T operands two d-tiles ahead of their
+        // MFMAs (left to itself the compiler issued each pair of transposing
+        // reads just before its MFMAs and waited for it)
+        const uint32_t kb0 = lds_address(base);
+        const uint32_t ae = kb0 + trl.even, ao = kb0 + trl.odd;
+        const uint32_t af = kb0 + (KCH + VCH) * 1024 + (j * 4 + col) * 16;
+        u32x4 f[FCH > 0 ? FCH : 1];
+        u32x2 x0[DT], x1[DT];
+        static_for<0, FCH>([&](auto ic) {
+          constexpr int ct = decltype(ic)::value;
+          f[ct] = ds_read_b128_asm<ct * 1024>(af);
+        });
+        auto rd = [&](auto ic) {
+          constexpr int dt = decltype(ic)::value;
+          const uint32_t a = (dt & 1) ? ao : ae;
+          x0[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024>(a);
+          x1[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024 + DP * 1024>(a);
+        };
+        rd(std::integral_constant<int, 0>{});
+        if constexpr (DT > 1) rd(std::integral_constant<int, 1>{});
+        static_for<0, FCH>([&](auto ic) {
+          constexpr int ct = decltype(ic)::value;
+          lgkm_fence<FCH - 1 - ct + 2 * (DT > 1 ? 2 : 1)>(f[ct]);
+          const uint4 a = __builtin_bit_cast(uint4, f[ct]);
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, bphi[qt], O[qt][ct]);
+        });
+        static_for<0, DT>([&](auto ic) {
+          constexpr int dt = decltype(ic)::value;
+          if constexpr (dt + 2 < DT) rd(std::integral_constant<int, dt + 2>{});
+          lgkm_fence<dt + 2 < DT ? 4 : dt + 1 < DT ? 2 : 0>(x0[dt], x1[dt]);
+          const uint4 a = uint4{x0[dt].x, x0[dt].y, x1[dt].x, x1[dt].y};
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
+        });
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
+        return;
       }
 #pragma unroll
       for (int ct = 0; ct < FCH; ++ct) {
@@ -929,18 +1007,6 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
       }
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
-      if constexpr (TR) {
-        // keep each transposing read two d-tiles ahead of its MFMAs (the
-        // scheduler would otherwise issue all of them first and spill)
-        __builtin_amdgcn_sched_group_barrier(0x100, FCH + 4, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, FCH * QT, 0);
-#pragma unroll
-        for (int dt = 0; dt + 2 < DT; ++dt) {
-          __builtin_amdgcn_sched_group_barrier(0x008, QT, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 2 * QT, 0);
-      }
       return;
     }
     uint4 ktr[DT];

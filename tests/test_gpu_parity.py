@@ -46,6 +46,7 @@ SHAPES = [
     # D > 128 with a fused forward-type sum: fp16 points take the K^T
     # operands by transposing reads of the key tiles, bf16 points a KS copy
     (90, 140, 200, 5, "bf16", "f32", "f32", None, 1.0),
+    (140, 260, 120, 8, "bf16", "f32", "f32", None, 1.0),
     (70, 530, 256, 16, "f16", "f16", "f32", None, 1.0),
     (96, 200, 256, 256, "f16", "f32", "f32", None, 1.0),
     (257, 97, 8, 64, "bf16", "f32", "f32", 0.5, 1.0),
