@@ -74,13 +74,14 @@ def oracle_ref(w, pas, rows=None, g=None):
         # before the magnitude) is kept for net_ratio
         fn = oracle.dq_scales if pas == "dq" else oracle.dk_scales
         val, absscale, net = fn(qv, kv, w.v, g, float(w.tau), rows=rows, threads=th)
-        NET_SCALES[id(val)] = net
+        NET_SCALES[id(val)] = (val, net)  # the array is held, so its id is not reused
         return val, absscale
     fn = {"dv": oracle.dv}[pas]
     return fn(qv, kv, w.v, g, float(w.tau), rows=rows, threads=th)
 
 
-# net scales of the gradient references oracle_ref returned, by id of the value array
+# (reference array, net scale) of the gradient references oracle_ref returned,
+# by id of the reference array
 NET_SCALES = {}
 
 
@@ -88,9 +89,10 @@ def net_ratio(got, ref):
     """max |gpu - oracle| / net scale over the elements whose net scale is at
     least 1e-3 of the row's largest (the other reading of the gradient
     tolerance; elements whose w cancel almost completely are left out)."""
-    net = NET_SCALES.get(id(ref))
-    if net is None or not net.size:
+    entry = NET_SCALES.get(id(ref))
+    if entry is None or entry[0] is not ref or not entry[1].size:
         return None
+    net = entry[1]
     err = np.abs(np.asarray(got, dtype=np.float64) - ref)
     keep = net >= 1e-3 * np.max(net, axis=1, keepdims=True)
     return float(np.max(np.where(keep, err / np.maximum(net, 1e-300), 0.0)))

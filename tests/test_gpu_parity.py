@@ -75,6 +75,38 @@ def test_small_shapes_all_outputs(shape):
     parity.check_workload(w, passes=("fwd", "dq"), fused=True)
 
 
+def _sweep_case(i):
+    """Seeded shape i of the random sweep: sizes from 1 to about 900 rows,
+    D from 1 to 256 (a third of the cases above 128, where the eight-wave
+    kernels with the three-phase step and the transposing K^T reads run),
+    C from 1 to 256 (mostly small, where the forward fuses into the
+    gradient passes), either point dtype, all value / gradient dtypes, and
+    tau from 0.05 / D to 4 / D."""
+    rng = np.random.default_rng(1000 + i)
+    M = int(rng.integers(1, 900))
+    N = int(rng.integers(1, 900))
+    band = i % 3
+    D = int(rng.integers(129, 257) if band == 0 else rng.integers(33, 129) if band == 1 else rng.integers(1, 33))
+    C = int(rng.choice([1, 2, 3, 5, 8, 15, 16, 17, 32, 64, 100, 128, 256]))
+    qk = "f16" if rng.random() < 0.6 else "bf16"
+    vd = str(rng.choice(["f32", "f16"]))
+    gd = str(rng.choice(["f32", "f16"]))
+    tau = float(np.exp(rng.uniform(np.log(0.05), np.log(4.0)))) / D
+    return M, N, D, C, qk, vd, gd, tau
+
+
+@pytest.mark.parametrize("i", range(18))
+def test_random_shape_sweep(i):
+    """Eighteen seeded random problems, every output of the separate and the
+    fused calls against the oracle on all rows."""
+    import parity
+    M, N, D, C, qk, vd, gd, tau = _sweep_case(i)
+    _say("sweep case", i, (M, N, D, C, qk, vd, gd, tau))
+    w = parity.random_workload(2000 + i, M, N, D, C, qk, vd, gd, tau)
+    stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
+    _say("  max err/A and rel-L2:", stats)
+
+
 def test_same_points_alias_matches_separate_arrays():
     import parity
     w = parity.random_workload(5, 300, 300, 24, 3, same=True)
