@@ -424,8 +424,9 @@ constexpr bool dq_transposed_keys(bool f16_points, int DP, int CW) {
 // 4g .. 4g+3) and of key tile 1 (second read: keys 16 + 4g .. +3), dimensions
 // 16 dt + 4c .. +3, through the XOR swizzle of the LDS columns.  The lane's
 // byte offsets within a chunk for even and odd dt (their 16-byte columns
-// differ by an XOR with 2) are computed once; everything else is an
-// immediate offset of the read.
+// differ by an XOR with 2) come from tr_lane; everything else is an
+// immediate offset of the read (chunk dt / 2 of key tile 0, and DP chunks
+// further for key tile 1).
 struct TrLane {
   int even, odd;
 };
@@ -434,17 +435,6 @@ __device__ __forceinline__ TrLane tr_lane(int lane) {
   const int row = 4 * g + r;
   const int col = (c >> 1) ^ ((row >> 1) & 3);
   return {row * 64 + col * 16 + (c & 1) * 8, row * 64 + (col ^ 2) * 16 + (c & 1) * 8};
-}
-template <int DP>
-__device__ __forceinline__ uint4 kt_operand_tr(const char* kbase, int dt, TrLane t) {
-  typedef short short4v __attribute__((ext_vector_type(4)));
-  typedef __attribute__((address_space(3))) short4v lds_short4v;
-  const char* p = kbase + ((dt & 1) ? t.odd : t.even) + (dt >> 1) * 1024;
-  const short4v a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)p);
-  const short4v b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4v*)(p + DP * 1024));
-  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-  const u32x2 ua = __builtin_bit_cast(u32x2, a), ub = __builtin_bit_cast(u32x2, b);
-  return uint4{ua.x, ua.y, ub.x, ub.y};
 }
 
 // LDS reads issued as assembly with immediate offsets, for operands that are
@@ -946,68 +936,63 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
         b[qt] = pack_tile_pair(p);
       }
       __builtin_amdgcn_sched_barrier(0);
-      // the lane's transposing-read offsets, formed again in every step from
-      // the lane index (an opaque instruction pair, so the compiler cannot
-      // keep them live across the loop, where they would cost registers)
-      TrLane trl{0, 0};
+      // The V^T tiles of the fused sum, then the K^T operands, read two
+      // d-tiles ahead of their MFMAs by assembly (left to itself the compiler
+      // issued each tile's reads just before its MFMAs and waited for them):
+      // two transposing reads of the RT key tiles per operand (TR; the lane's
+      // offsets formed again in every step from the lane index by an opaque
+      // instruction pair, so the compiler cannot keep them live across the
+      // loop, where they would cost registers), else one read of the KS copy.
+      constexpr int RPT = TR ? 2 : 1;  // reads per d-tile
+      const uint32_t kb0 = lds_address(base);
+      const uint32_t lo = kb0 + (j * 4 + col) * 16;  // the lane's operand column
+      uint32_t ae = lo, ao = lo;
       if constexpr (TR) {
         int ln;
         asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
-        trl = tr_lane(ln);
-        // the V^T tiles, then the K^T operands two d-tiles ahead of their
-        // MFMAs (left to itself the compiler issued each pair of transposing
-        // reads just before its MFMAs and waited for it)
-        const uint32_t kb0 = lds_address(base);
-        const uint32_t ae = kb0 + trl.even, ao = kb0 + trl.odd;
-        const uint32_t af = kb0 + (KCH + VCH) * 1024 + (j * 4 + col) * 16;
-        u32x4 f[FCH > 0 ? FCH : 1];
-        u32x2 x0[DT], x1[DT];
-        static_for<0, FCH>([&](auto ic) {
-          constexpr int ct = decltype(ic)::value;
-          f[ct] = ds_read_b128_asm<ct * 1024>(af);
-        });
-        auto rd = [&](auto ic) {
-          constexpr int dt = decltype(ic)::value;
+        const TrLane trl = tr_lane(ln);
+        ae = kb0 + trl.even;
+        ao = kb0 + trl.odd;
+      }
+      u32x4 f[FCH > 0 ? FCH : 1];
+      u32x2 x0[DT], x1[DT];
+      static_for<0, FCH>([&](auto ic) {
+        constexpr int ct = decltype(ic)::value;
+        f[ct] = ds_read_b128_asm<(KCH + VCH + TCH + ct) * 1024>(lo);
+      });
+      auto rd = [&](auto ic) {
+        constexpr int dt = decltype(ic)::value;
+        if constexpr (TR) {
           const uint32_t a = (dt & 1) ? ao : ae;
           x0[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024>(a);
           x1[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024 + DP * 1024>(a);
-        };
-        rd(std::integral_constant<int, 0>{});
-        if constexpr (DT > 1) rd(std::integral_constant<int, 1>{});
-        static_for<0, FCH>([&](auto ic) {
-          constexpr int ct = decltype(ic)::value;
-          lgkm_fence<FCH - 1 - ct + 2 * (DT > 1 ? 2 : 1)>(f[ct]);
-          const uint4 a = __builtin_bit_cast(uint4, f[ct]);
-#pragma unroll
-          for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, bphi[qt], O[qt][ct]);
-        });
-        static_for<0, DT>([&](auto ic) {
-          constexpr int dt = decltype(ic)::value;
-          if constexpr (dt + 2 < DT) rd(std::integral_constant<int, dt + 2>{});
-          lgkm_fence<dt + 2 < DT ? 4 : dt + 1 < DT ? 2 : 0>(x0[dt], x1[dt]);
-          const uint4 a = uint4{x0[dt].x, x0[dt].y, x1[dt].x, x1[dt].y};
-#pragma unroll
-          for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
-        });
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
-        return;
-      }
-#pragma unroll
-      for (int ct = 0; ct < FCH; ++ct) {
-        const uint4 a = fb[(16 * ct + j) * 4 + col];
+        } else {
+          const u32x4 r = ds_read_b128_asm<(KCH + VCH + dt) * 1024>(lo);
+          x0[dt] = u32x2{r.x, r.y};
+          x1[dt] = u32x2{r.z, r.w};
+        }
+      };
+      constexpr int LT = DT > 1 ? 2 : 1;  // d-tiles read ahead
+      static_for<0, LT>(rd);
+      static_for<0, FCH>([&](auto ic) {
+        constexpr int ct = decltype(ic)::value;
+        lgkm_fence<FCH - 1 - ct + RPT * LT>(f[ct]);
+        const uint4 a = __builtin_bit_cast(uint4, f[ct]);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, bphi[qt], O[qt][ct]);
-      }
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const uint4 a = TR ? kt_operand_tr<DP>(base, dt, trl) : tb[(16 * dt + j) * 4 + col];
+      });
+      static_for<0, DT>([&](auto ic) {
+        constexpr int dt = decltype(ic)::value;
+        if constexpr (dt + LT < DT) rd(std::integral_constant<int, dt + LT>{});
+        lgkm_fence<RPT * (dt + LT < DT ? LT : DT - 1 - dt)>(x0[dt], x1[dt]);
+        const uint4 a = uint4{x0[dt].x, x0[dt].y, x1[dt].x, x1[dt].y};
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
-      }
+      });
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
       return;
+
     }
     uint4 ktr[DT];
 #pragma unroll
