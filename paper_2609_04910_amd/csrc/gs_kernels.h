@@ -936,47 +936,70 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
         b[qt] = pack_tile_pair(p);
       }
       __builtin_amdgcn_sched_barrier(0);
-      // The V^T tiles of the fused sum, then the K^T operands, read two
-      // d-tiles ahead of their MFMAs by assembly (left to itself the compiler
-      // issued each tile's reads just before its MFMAs and waited for them):
-      // two transposing reads of the RT key tiles per operand (TR; the lane's
-      // offsets formed again in every step from the lane index by an opaque
-      // instruction pair, so the compiler cannot keep them live across the
-      // loop, where they would cost registers), else one read of the KS copy.
-      constexpr int RPT = TR ? 2 : 1;  // reads per d-tile
-      const uint32_t kb0 = lds_address(base);
-      const uint32_t lo = kb0 + (j * 4 + col) * 16;  // the lane's operand column
-      uint32_t ae = lo, ao = lo;
+      // the lane's transposing-read offsets, formed again in every step from
+      // the lane index (an opaque instruction pair, so the compiler cannot
+      // keep them live across the loop, where they would cost registers)
+      TrLane trl{0, 0};
       if constexpr (TR) {
         int ln;
         asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
-        const TrLane trl = tr_lane(ln);
-        ae = kb0 + trl.even;
-        ao = kb0 + trl.odd;
+        trl = tr_lane(ln);
+        // the V^T tiles, then the K^T operands two d-tiles ahead of their
+        // MFMAs (left to itself the compiler issued each pair of transposing
+        // reads just before its MFMAs and waited for it)
+        const uint32_t kb0 = lds_address(base);
+        const uint32_t ae = kb0 + trl.even, ao = kb0 + trl.odd;
+        const uint32_t af = kb0 + (KCH + VCH) * 1024 + (j * 4 + col) * 16;
+        u32x4 f[FCH > 0 ? FCH : 1];
+        u32x2 x0[DT], x1[DT];
+        static_for<0, FCH>([&](auto ic) {
+          constexpr int ct = decltype(ic)::value;
+          f[ct] = ds_read_b128_asm<ct * 1024>(af);
+        });
+        auto rd = [&](auto ic) {
+          constexpr int dt = decltype(ic)::value;
+          const uint32_t a = (dt & 1) ? ao : ae;
+          x0[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024>(a);
+          x1[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024 + DP * 1024>(a);
+        };
+        rd(std::integral_constant<int, 0>{});
+        if constexpr (DT > 1) rd(std::integral_constant<int, 1>{});
+        static_for<0, FCH>([&](auto ic) {
+          constexpr int ct = decltype(ic)::value;
+          lgkm_fence<FCH - 1 - ct + 2 * (DT > 1 ? 2 : 1)>(f[ct]);
+          const uint4 a = __builtin_bit_cast(uint4, f[ct]);
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, bphi[qt], O[qt][ct]);
+        });
+        static_for<0, DT>([&](auto ic) {
+          constexpr int dt = decltype(ic)::value;
+          if constexpr (dt + 2 < DT) rd(std::integral_constant<int, dt + 2>{});
+          lgkm_fence<dt + 2 < DT ? 4 : dt + 1 < DT ? 2 : 0>(x0[dt], x1[dt]);
+          const uint4 a = uint4{x0[dt].x, x0[dt].y, x1[dt].x, x1[dt].y};
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
+        });
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
+        return;
       }
-      u32x4 f[FCH > 0 ? FCH : 1];
-      u32x2 x0[DT], x1[DT];
+      // bf16 points: the V^T tiles, then the K^T operands from the KS copy,
+      // also two d-tiles ahead of their MFMAs
+      const uint32_t lo = lds_address(base) + (j * 4 + col) * 16;  // the lane's operand column
+      u32x4 f[FCH > 0 ? FCH : 1], x[DT];
       static_for<0, FCH>([&](auto ic) {
         constexpr int ct = decltype(ic)::value;
         f[ct] = ds_read_b128_asm<(KCH + VCH + TCH + ct) * 1024>(lo);
       });
       auto rd = [&](auto ic) {
         constexpr int dt = decltype(ic)::value;
-        if constexpr (TR) {
-          const uint32_t a = (dt & 1) ? ao : ae;
-          x0[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024>(a);
-          x1[dt] = ds_read_tr_b64_asm<(dt >> 1) * 1024 + DP * 1024>(a);
-        } else {
-          const u32x4 r = ds_read_b128_asm<(KCH + VCH + dt) * 1024>(lo);
-          x0[dt] = u32x2{r.x, r.y};
-          x1[dt] = u32x2{r.z, r.w};
-        }
+        x[dt] = ds_read_b128_asm<(KCH + VCH + dt) * 1024>(lo);
       };
-      constexpr int LT = DT > 1 ? 2 : 1;  // d-tiles read ahead
+      constexpr int LT = DT > 1 ? 2 : 1;
       static_for<0, LT>(rd);
       static_for<0, FCH>([&](auto ic) {
         constexpr int ct = decltype(ic)::value;
-        lgkm_fence<FCH - 1 - ct + RPT * LT>(f[ct]);
+        lgkm_fence<FCH - 1 - ct + LT>(f[ct]);
         const uint4 a = __builtin_bit_cast(uint4, f[ct]);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, bphi[qt], O[qt][ct]);
@@ -984,15 +1007,14 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
       static_for<0, DT>([&](auto ic) {
         constexpr int dt = decltype(ic)::value;
         if constexpr (dt + LT < DT) rd(std::integral_constant<int, dt + LT>{});
-        lgkm_fence<RPT * (dt + LT < DT ? LT : DT - 1 - dt)>(x0[dt], x1[dt]);
-        const uint4 a = uint4{x0[dt].x, x0[dt].y, x1[dt].x, x1[dt].y};
+        lgkm_fence<dt + LT < DT ? LT : DT - 1 - dt>(x[dt]);
+        const uint4 a = __builtin_bit_cast(uint4, x[dt]);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
       });
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
       return;
-
     }
     uint4 ktr[DT];
 #pragma unroll
