@@ -899,7 +899,7 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
     if constexpr (PHASED) {
       // all score MFMAs (A operands read chunk by chunk, each feeding every
       // query tile), then the w contractions, exponentials and products, then
-      // the contractions over keys with their A operands read as they are used
+      // the contractions over keys, their A operands read two d-tiles ahead
       floatx4 acc[QT][2];
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt)
