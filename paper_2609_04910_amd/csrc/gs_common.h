@@ -136,6 +136,18 @@ __device__ __forceinline__ int scale_exponent(uint32_t max_bits) {
   return 1 - e;
 }
 
+// Exponent of the scale of the fp16 KS copy of bf16 points (the operand of
+// the gradient contraction): the largest magnitude lands in [2^14, 2^15), so
+// coordinates down to 2^-28 of it keep fp16's full 11 bits.  Scaled to
+// [1, 2), as the values are, coordinates below 2^-14 of the largest fell
+// into fp16 subnormals, and where such a coordinate of q nearly equals the
+// same coordinate of k the difference q - k, which the gradient sums, lost
+// its leading bits.
+constexpr int kPointScaleHeadroom = 14;
+__device__ __forceinline__ int point_scale_exponent(uint32_t max_bits) {
+  return scale_exponent(max_bits) + kPointScaleHeadroom;
+}
+
 // Per-problem byte strides of a launch over a batch of problems: problem
 // blockIdx.z finds each operand at its base + blockIdx.z * stride.  One
 // problem: all zero, gridDim.z = 1.

@@ -1093,7 +1093,7 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   };
   key_stream<NS, NCH + 1>(s_begin, s_end, issue, compute);
 
-  const int ek = kslot ? scale_exponent(*kslot) : 0;
+  const int ek = kslot ? point_scale_exponent(*kslot) : 0;
   const uint16_t* q16 = reinterpret_cast<const uint16_t*>(qs);
   // rs holds this lane's 8-key partial sums; add the other three key groups
 #pragma unroll

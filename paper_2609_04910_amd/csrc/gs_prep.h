@@ -162,8 +162,8 @@ __global__ void k_points_rt_norm(const uint16_t* __restrict__ x, int64_t n, int 
     (void)rt_norm_item<T>(x, n, D, W, xs, nh, vec, t);
 }
 
-// Points, KS-layout fp16 copy scaled by 2^e (e from *slot when slot != NULL,
-// needed for bf16 inputs whose range exceeds fp16) and, when sgn != NULL,
+// Points, KS-layout fp16 copy scaled by 2^e (e = point_scale_exponent(*slot)
+// when slot != NULL, for bf16 inputs whose range exceeds fp16) and, when sgn != NULL,
 // multiplied by the sign of the single-channel value sgn[r] (exact).  Thread
 // (32-key block, row w, quarter a) writes the eight key slots 8a .. 8a+7 of
 // row w (one 16-byte store); consecutive threads write consecutive 16 bytes.
@@ -176,7 +176,7 @@ __global__ void k_points_ks(const uint16_t* __restrict__ x, int64_t n, int D, in
   sgn = zoff(sgn, bz.in2);
   xt = zoff(xt, bz.ws);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const float s = slot ? ldexpf(1.0f, scale_exponent(*slot)) : 1.0f;
+  const float s = slot ? ldexpf(1.0f, point_scale_exponent(*slot)) : 1.0f;
   const int64_t total = (n_pad >> 5) * R * 4;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += stride) {
     const int a = (int)(t & 3);

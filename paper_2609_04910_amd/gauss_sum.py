@@ -65,13 +65,23 @@ class Problem(ctypes.Structure):
 _lib = None
 
 
-def load(path=LIB_PATH):
-    """Load libgauss_sum.so (built in-tree by ``__graft_entry__.build()``)."""
+def load(path=LIB_PATH, torch_runtime=True):
+    """Load libgauss_sum.so (built in-tree by ``__graft_entry__.build()``).
+
+    torch is imported first (torch_runtime): PyTorch for ROCm ships its own
+    HIP runtime, loaded under the unversioned name libamdhip64.so, while
+    the library asks for libamdhip64.so.7.  With torch's copy already in the
+    process that request binds to it; the other way round the process holds
+    two HIP runtimes, and torch's streams and allocations are not valid in
+    the library's, so every call fails with GS_ERR_HIP.  Callers of the C
+    ABI without torch are not affected."""
     global _lib
     if _lib is not None and path == LIB_PATH:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError("HIP library %s is missing: run __graft_entry__.build() first" % path)
+    if torch_runtime:
+        import torch  # noqa: F401  (its HIP runtime first, see above)
     lib = ctypes.CDLL(path)
     vp, sz, f32p = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p
     P = ctypes.POINTER(Problem)

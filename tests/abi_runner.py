@@ -12,7 +12,7 @@ sys.path.insert(0, HERE)
 from paper_2609_04910_amd import gauss_sum as gs  # noqa: E402
 
 gs.LIB_PATH = sys.argv[1]
-gs.load.__defaults__ = (sys.argv[1],)
+gs.load.__defaults__ = (sys.argv[1], False)  # no torch in the sanitizer run
 
 import pytest  # noqa: E402
 

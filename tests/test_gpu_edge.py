@@ -105,3 +105,30 @@ def test_value_and_gradient_magnitudes_near_1e4(vdt):
     assert np.max(np.abs(w.v.astype(np.float32))) > 2e4
     stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
     _say("  stats", stats)
+
+
+@pytest.mark.parametrize("tiny", [1e-5, 1e-7])
+def test_bf16_points_with_a_tiny_coordinate(tiny):
+    """bf16 points whose last coordinate is `tiny` times the others: the fp16
+    copy that the gradient contraction reads is scaled so its largest
+    magnitude lies in [2^14, 2^15), and the tiny coordinate keeps its 11
+    bits.  Scaled to [1, 2), as before, it fell into fp16 subnormals, and the
+    gradients' last coordinate (a sum of the small differences q - k there)
+    was off by 4.8e-4 / 5.2e-4 of its scale (dq / dk) at 1e-5, 2.6e-2 /
+    3.1e-2 at 1e-7; now 3.9e-5 / 5.0e-5 at either."""
+    import parity
+    rng = np.random.default_rng(11)
+    M, N, D, C = 300, 500, 16, 4
+    x = rng.standard_normal((M, D)).astype(np.float32)
+    y = rng.standard_normal((N, D)).astype(np.float32)
+    x[:, -1] *= np.float32(tiny)
+    y[:, -1] *= np.float32(tiny)
+    q, qv = wl.bf16_round(x)
+    k, kv = wl.bf16_round(y)
+    v = rng.standard_normal((N, C)).astype(np.float32)
+    g = rng.standard_normal((M, C)).astype(np.float32)
+    w = wl.Workload("tiny%g" % tiny, M, N, D, C, np.float32(1.0 / D), "bf16", q, k, v, g,
+                    ("fwd", "dq", "dk", "dv"), False, qv, kv)
+    _say("bf16 points, last coordinate scaled by", tiny)
+    stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
+    _say("  stats", stats)
