@@ -730,15 +730,20 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
       for (int ct = 0; ct < CT; ++ct) O[qt][ct] = mfma_f16(vr[ct], b, O[qt][ct]);
     }
   };
+  auto stream = [&](auto cmp) {
+    // eight waves and four stages: one barrier per two steps (not at
+    // D = 256, where the two steps' code spills in the loop)
+    if constexpr (WIDE && NS == 4 && DP <= 4)
+      key_stream_pairs<NCH + 1>(s_begin, s_end, issue, cmp);
+    else
+      key_stream<NS, NCH + 1>(s_begin, s_end, issue, cmp);
+  };
   if (level == 2)
-    key_stream<NS, NCH + 1>(s_begin, s_end, issue,
-                            [&](int st) { compute(st, std::integral_constant<int, 2>{}); });
+    stream([&](int st) { compute(st, std::integral_constant<int, 2>{}); });
   else if (shifted)
-    key_stream<NS, NCH + 1>(s_begin, s_end, issue,
-                            [&](int st) { compute(st, std::integral_constant<int, 1>{}); });
+    stream([&](int st) { compute(st, std::integral_constant<int, 1>{}); });
   else
-    key_stream<NS, NCH + 1>(s_begin, s_end, issue,
-                            [&](int st) { compute(st, std::integral_constant<int, 0>{}); });
+    stream([&](int st) { compute(st, std::integral_constant<int, 0>{}); });
 
   const int ev = scale_exponent(*vslot) - (ONE ? 1 : 0);
   const bool v4 = vec4_rows(out, C);
