@@ -460,6 +460,16 @@ __device__ __forceinline__ TrLane tr_lane(int lane) {
   return {row * 64 + col * 16 + (c & 1) * 8, row * 64 + (col ^ 2) * 16 + (c & 1) * 8};
 }
 
+// The lane index formed by an opaque instruction pair: values derived from
+// it inside a key step are formed again in every step instead of being kept
+// live across the key loop (where, short of registers, the compiler would
+// otherwise spill them and reload them from scratch memory in every step).
+__device__ __forceinline__ int opaque_lane() {
+  int ln;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+  return ln;
+}
+
 // LDS reads issued as assembly with immediate offsets, for operands that are
 // read well ahead of their use: the compiler neither sinks such a read to its
 // first use nor counts it in its own waits, so the reader waits explicitly
@@ -581,7 +591,10 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
     for (int c = 0; c < KCH; ++c) dma_x4(rk, (ls * KCH + c) * 1024, base + c * 1024, dlane);
 #pragma unroll
     for (int c = 0; c < CT; ++c) dma_x4(rv, (ls * CT + c) * 1024, base + (KCH + c) * 1024, dlane);
-    dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024, 4 * lane);
+    // at D > 128 with one value tile the scalar row's lane offset is formed
+    // again in every step (kept live across the loop it was spilled)
+    dma_x1(rsc, ls * kScalarFloats * 4, base + NCH * 1024,
+           4 * (DP == 8 && CT == 1 ? opaque_lane() : lane));
   };
 
   uint4 qreg[QT][DP];
@@ -911,18 +924,26 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
     const uint4* vb = reinterpret_cast<const uint4*>(base + KCH * 1024);
     const uint4* tb = reinterpret_cast<const uint4*>(base + (KCH + VCH) * 1024);
     const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
+    // the lane's tile row and column group: in the SVGD mode formed again in
+    // every step (kept live across the loop they pushed a spill into it)
+    int jl = j, gl = g;
+    if constexpr (SV) {
+      const int ln = opaque_lane();
+      jl = ln & 15;
+      gl = ln >> 4;
+    }
     floatx4 cin[2];
     uint4 kr[2][DP];
     uint4 vr[2][GW];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-      cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
-      if constexpr (!PHASED) load_k_tile_lds<DP>(kb, kt, j, g, kr[kt]);
-      if constexpr (CW > 0) load_k_tile_lds<GW>(vb, kt, j, g, vr[kt]);
+      cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * gl);
+      if constexpr (!PHASED) load_k_tile_lds<DP>(kb, kt, jl, gl, kr[kt]);
+      if constexpr (CW > 0) load_k_tile_lds<GW>(vb, kt, jl, gl, vr[kt]);
     }
     // per key slot of this lane's B operand: sign(v_n) (single channel) or 1
     const uint4 sg = (CW > 0 || SV) ? uint4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u}
-                                    : *reinterpret_cast<const uint4*>(sc + 32 + 4 * g);
+                                    : *reinterpret_cast<const uint4*>(sc + 32 + 4 * gl);
     const uint4* fb = reinterpret_cast<const uint4*>(base + (KCH + VCH + TCH) * 1024);
     if constexpr (PHASED) {
       // all score MFMAs (A operands read chunk by chunk, each feeding every
@@ -964,14 +985,11 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
         b[qt] = pack_tile_pair(p);
       }
       __builtin_amdgcn_sched_barrier(0);
-      // the lane's transposing-read offsets, formed again in every step from
-      // the lane index (an opaque instruction pair, so the compiler cannot
-      // keep them live across the loop, where they would cost registers)
+      // the lane's transposing-read offsets, formed again in every step (kept
+      // live across the loop they would cost registers)
       TrLane trl{0, 0};
       if constexpr (TR) {
-        int ln;
-        asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
-        trl = tr_lane(ln);
+        trl = tr_lane(opaque_lane());
         // the V^T tiles, then the K^T operands two d-tiles ahead of their
         // MFMAs (left to itself the compiler issued each pair of transposing
         // reads just before its MFMAs and waited for it)
@@ -1046,10 +1064,10 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
     }
     uint4 ktr[DT];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + j) * 4 + lds_col(j, g)];
+    for (int dt = 0; dt < DT; ++dt) ktr[dt] = tb[(16 * dt + jl) * 4 + lds_col(jl, gl)];
     uint4 vtr[FCH > 0 ? FCH : 1];
 #pragma unroll
-    for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + j) * 4 + lds_col(j, g)];
+    for (int ct = 0; ct < FCH; ++ct) vtr[ct] = fb[(16 * ct + jl) * 4 + lds_col(jl, gl)];
     if constexpr (CW == 0) {
       // single channel: the score MFMAs of all query tiles, then their
       // exponentials, then the contractions over keys, kept apart by
