@@ -65,7 +65,11 @@ def run(xs, score, tau):
 
 @pytest.mark.parametrize("N,D,qk,sdt,tau", [
     (1, 4, "f16", "f32", 0.5), (300, 64, "f16", "f32", 1.0 / 64), (777, 128, "f16", "f16", 1.0 / 128),
-    (1000, 32, "bf16", "f32", 1.0 / 32), (517, 17, "f16", "f32", 0.3)])
+    (1000, 32, "bf16", "f32", 1.0 / 32), (517, 17, "f16", "f32", 0.3),
+    # the D > 128 instance (one query tile per wave, 16 tiles of score values)
+    # and bf16 points beyond D = 32
+    (400, 256, "f16", "f32", 1.0 / 256), (350, 200, "bf16", "f16", 1.0 / 200),
+    (640, 100, "bf16", "f32", 1.0 / 100)])
 def test_svgd_matches_oracle(N, D, qk, sdt, tau):
     xs, xv, score = particles(N + D, N, D, qk, sdt)
     got = run(xs, score, tau)
