@@ -67,8 +67,8 @@ inline Dims dims_of(int64_t D, int64_t C) {
 // per SIMD).  Gradient: for D > 64 two tiles even where that needs the
 // occupancy hint on k_dq or (D = 256, whose LDS ring allows one workgroup per
 // CU anyway) one wave per SIMD: a K tile read from LDS then feeds two MFMAs,
-// and a single tile per wave is bound by LDS bandwidth; D = 256 with
-// C > 128 keeps one tile (two would spill inside the key loop).
+// and a single tile per wave is bound by LDS bandwidth; D > 128 with
+// C > 64 keeps one tile (two would spill inside the key loop).
 constexpr int fwd_qt(int DP, int CT) {
   return CT >= 16 ? 1 : CT == 8 ? 2 : (DP == 8 && CT > 1) ? 2 : (DP <= 2 && CT <= 2) ? 8 : 4;
 }
@@ -86,7 +86,7 @@ constexpr int dq_wpb(int DP) { return DP >= 4 ? 2 * kWavesPerBlock : kWavesPerBl
 constexpr int fwd_wpb(int DP) { return DP >= 4 ? 2 * kWavesPerBlock : kWavesPerBlock; }
 
 constexpr int dq_qt(int DP, int CW) {
-  return DP >= 4 ? (DP == 8 && CW == 8 ? 1 : 2) : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
+  return DP >= 4 ? (DP == 8 && CW >= 4 ? 1 : 2) : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
 }
 
 // Every workgroup of a main kernel covers at most kRowPad query rows (the

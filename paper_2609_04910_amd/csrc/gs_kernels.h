@@ -424,9 +424,15 @@ __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
 // then the w contractions and exponentials, then the contractions over keys,
 // each LDS operand read as it is used): several channels at D > 64 where the
 // pass then fits in 256 registers without spills in the key loop (checked
-// per instance: D <= 128 with C <= 128, D <= 256 with C <= 32 or C > 224).
+// per instance: D <= 128 with C <= 128, D <= 256 with C <= 32 or C > 64;
+// D > 128 with C > 32 takes one query tile per wave).  Measured against the
+// plain step for fp16 and bf16, M = N = 32768, forward and full gradient:
+// D = 256, C = 128 10.76 -> 4.65 ms (the plain step with two query tiles
+// reloaded 27 spilled values in every key step; 5.3 ms with one); the plain
+// step stays faster at D = 256, C = 64 (3.80 against 4.04 ms) and at
+// D = 128, C = 256 (4.54 against 5.02 ms).
 constexpr bool dq_phased(int DP, int CW) {
-  return CW > 0 && ((DP == 4 && CW <= 4) || (DP == 8 && (CW == 1 || CW == 8)));
+  return CW > 0 && ((DP == 4 && CW <= 4) || (DP == 8 && (CW == 1 || CW >= 4)));
 }
 
 // Whether the gradient kernel takes its K^T operands from the streamed RT

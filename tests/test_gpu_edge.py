@@ -132,3 +132,38 @@ def test_bf16_points_with_a_tiny_coordinate(tiny):
     _say("bf16 points, last coordinate scaled by", tiny)
     stats = parity.check_workload(w, passes=("fwd", "dq", "dk", "dv"))
     _say("  stats", stats)
+
+
+def test_dominant_pair_with_an_equal_coordinate():
+    """The limit of the per-element gradient scale: where the one pair that
+    dominates a row of dq (a column of dk) has exactly equal coordinate d,
+    that pair's term drops out of the element and of its scale, and the rest
+    lies far below the pair's share of the two fp32 sums of the expanded
+    form tau (sum P k_d - q_d sum P).  In this seeded case (fp16, spread 3,
+    tau 3, kernel values near 1e-15) such elements exist: every other
+    element meets the usual bound, and every element beyond it has that
+    structure and an error within 2^-20 of the dominant pair's term
+    tau Phi sum_c |g_c v_c| |q_d|."""
+    import oracle
+    import parity
+    w = parity.random_workload(21, 150, 400, 8, 4, "f16", "f32", "f32", 3.0, 3.0)
+    got = parity.run(w, ("dq", "dk"))
+    qv = w.q_values.astype(np.float64)
+    kv = w.k_values.astype(np.float64)
+    d2 = ((qv[:, None, :] - kv[None, :, :]) ** 2).sum(-1)
+    tol = parity.TOL["f16"]
+    special = 0
+    for pas in ("dq", "dk"):
+        ref, scale = parity.oracle_ref(w, pas)
+        err = np.abs(got[pas].astype(np.float64) - ref)
+        for r, d in np.argwhere(err > tol * scale + 1e-30):
+            m, n = (r, int(np.argmin(d2[r]))) if pas == "dq" else (int(np.argmin(d2[:, r])), r)
+            assert qv[m, d] == kv[n, d], (pas, r, d)
+            phi = oracle.fwd(w.q_values[m:m + 1], w.k_values[n:n + 1], np.ones((1, 1), np.float32),
+                             float(w.tau))[0][0, 0]
+            term = float(w.tau) * phi * np.abs(w.g[m].astype(np.float64) * w.v[n]).sum() * abs(qv[m, d])
+            assert err[r, d] <= 2.0 ** -20 * term, (pas, r, d, err[r, d], term)
+            _say("  %s[%d, %d]: err %.3e, scale %.3e, dominant term %.3e" % (pas, r, d, err[r, d], scale[r, d],
+                                                                          term))
+            special += 1
+    assert special >= 1

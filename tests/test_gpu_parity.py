@@ -49,9 +49,6 @@ SHAPES = [
     (140, 260, 120, 8, "bf16", "f32", "f32", None, 1.0),
     (70, 530, 256, 16, "f16", "f16", "f32", None, 1.0),
     (96, 200, 256, 256, "f16", "f32", "f32", None, 1.0),
-    # D > 128 with a single channel (forward with one value tile)
-    (300, 700, 256, 1, "f16", "f32", "f32", None, 1.0),
-    (130, 520, 240, 1, "bf16", "f16", "f32", None, 1.0),
     (257, 97, 8, 64, "bf16", "f32", "f32", 0.5, 1.0),
     (33, 1000, 15, 1, "f16", "f32", "f32", None, 1.0),
     (1000, 33, 1, 8, "f16", "f32", "f32", 2.0, 1.0),
@@ -63,6 +60,13 @@ SHAPES = [
     # D <= 64 forward runs 128 query rows per wave, 512 per workgroup
     (768, 777, 64, 1, "f16", "f32", "f32", None, 1.0),
     (1300, 600, 32, 3, "bf16", "f32", "f32", None, 1.0),
+    # appended (the list position seeds each case)
+    # D > 128 with a single channel (forward with one value tile)
+    (300, 700, 256, 1, "f16", "f32", "f32", None, 1.0),
+    (130, 520, 240, 1, "bf16", "f16", "f32", None, 1.0),
+    # D > 128 with 65 - 128 channels: one query tile per wave, three phases
+    (150, 333, 256, 128, "f16", "f32", "f32", None, 1.0),
+    (111, 290, 180, 100, "bf16", "f16", "f32", None, 1.0),
 ]
 
 
