@@ -843,6 +843,12 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   // fits (and the fused forward costs a few per cent of the pass instead of
   // a pass of its own)
   constexpr bool PHASED = dq_phased(DP, CW);
+  // the SVGD mode at D > 128: every LDS operand read as it is used (held
+  // for the whole step, the 16 K^T and 16 score tiles with the score
+  // operands spilled 23 values per key step: N = 16384, D = 256 1.84 ->
+  // 0.63 ms per call, bitwise identical; at D <= 128, where nothing spills,
+  // reading as used measured 1 - 3 % slower)
+  constexpr bool LAZY = SV && DP == 8;
   // K^T operands read from the RT key tiles by transposing LDS reads (no KS
   // copy of the keys in the stream)
   constexpr bool TR = dq_transposed_keys(std::is_same<T, F16>::value, DP, CW);
@@ -944,7 +950,7 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * gl);
-      if constexpr (!PHASED) load_k_tile_lds<DP>(kb, kt, jl, gl, kr[kt]);
+      if constexpr (!PHASED && !LAZY) load_k_tile_lds<DP>(kb, kt, jl, gl, kr[kt]);
       if constexpr (CW > 0) load_k_tile_lds<GW>(vb, kt, jl, gl, vr[kt]);
     }
     // per key slot of this lane's B operand: sign(v_n) (single channel) or 1
@@ -1064,6 +1070,53 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
       });
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
+      return;
+    }
+    if constexpr (LAZY) {
+      const int cl = lds_col(jl, gl);
+      floatx4 acc[QT][2];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) acc[qt][kt] = cin[kt];
+#pragma unroll
+      for (int dc = 0; dc < DP; ++dc) {
+        const uint4 a0 = kb[(dc * 16 + jl) * 4 + cl];
+        const uint4 a1 = kb[((DP + dc) * 16 + jl) * 4 + cl];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          acc[qt][0] = mfma_qk<T>(a0, qreg[qt][dc], acc[qt][0]);
+          acc[qt][1] = mfma_qk<T>(a1, qreg[qt][dc], acc[qt][1]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      uint4 b[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        float p[2][4];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) p[kt][r] = exp2_clamped(fmaf(acc[qt][kt][r], tau2, bq[qt]));
+        b[qt] = pack_tile_pair(p);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const uint4 a = tb[(16 * dt + jl) * 4 + cl];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) dQ[qt][dt] = mfma_f16(a, b[qt], dQ[qt][dt]);
+        if ((dt & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int ct = 0; ct < FCH; ++ct) {
+        const uint4 a = fb[(16 * ct + jl) * 4 + cl];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, b[qt], O[qt][ct]);
+        if ((ct & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) rs[qt] = dot2_acc(b[qt], sg, rs[qt]);
       return;

@@ -69,7 +69,7 @@ def run(xs, score, tau):
     # the D > 128 instance (one query tile per wave, 16 tiles of score values)
     # and bf16 points beyond D = 32
     (400, 256, "f16", "f32", 1.0 / 256), (350, 200, "bf16", "f16", 1.0 / 200),
-    (640, 100, "bf16", "f32", 1.0 / 100)])
+    (640, 100, "bf16", "f32", 1.0 / 100), (1000, 129, "f16", "f16", 1.0 / 129)])
 def test_svgd_matches_oracle(N, D, qk, sdt, tau):
     xs, xv, score = particles(N + D, N, D, qk, sdt)
     got = run(xs, score, tau)
