@@ -843,12 +843,16 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   // fits (and the fused forward costs a few per cent of the pass instead of
   // a pass of its own)
   constexpr bool PHASED = dq_phased(DP, CW);
-  // the SVGD mode at D > 128: every LDS operand read as it is used (held
-  // for the whole step, the 16 K^T and 16 score tiles with the score
-  // operands spilled 23 values per key step: N = 16384, D = 256 1.84 ->
-  // 0.63 ms per call, bitwise identical; at D <= 128, where nothing spills,
-  // reading as used measured 1 - 3 % slower)
-  constexpr bool LAZY = SV && DP == 8;
+  // the single-channel step and the SVGD mode at D > 128: every LDS operand
+  // read as it is used.  Held for the whole step, the score operands and
+  // the 16 K^T tiles (and the SVGD mode's 16 score tiles) spilled inside
+  // the key loop: SVGD N = 16384, D = 256 1.84 -> 0.63 ms per call; the
+  // single-channel gradient fits two query tiles in 244 registers this way
+  // (D = 256, C = 1, M = 32768, N = 65536, forward and full gradient: two
+  // tiles held 9.27 ms, one tile held 5.86 ms, two tiles read as used
+  // 3.96 ms).  At D <= 128, where nothing spills, reading as used measured
+  // 1 - 3 % slower (SVGD mode).
+  constexpr bool LAZY = (SV || CW == 0) && DP == 8;
   // K^T operands read from the RT key tiles by transposing LDS reads (no KS
   // copy of the keys in the stream)
   constexpr bool TR = dq_transposed_keys(std::is_same<T, F16>::value, DP, CW);

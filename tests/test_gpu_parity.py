@@ -62,7 +62,7 @@ SHAPES = [
     (1300, 600, 32, 3, "bf16", "f32", "f32", None, 1.0),
     # appended (the list position seeds each case)
     # D > 128 with a single channel (forward with one value tile, gradient
-    # with one query tile per wave)
+    # with its LDS operands read as they are used)
     (300, 700, 256, 1, "f16", "f32", "f32", None, 1.0),
     (130, 520, 240, 1, "bf16", "f16", "f32", None, 1.0),
     # D > 128 with 65 - 128 channels: one query tile per wave, three phases
