@@ -683,13 +683,68 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
     const float* sc = reinterpret_cast<const float*>(base + NCH * 1024);
     floatx4 cin[2];
     uint4 kr[2][DP];
+    // D > 128 with eight or more value tiles: all score MFMAs (each K read
+    // feeding every query tile), then the exponentials, then the value
+    // contractions, every LDS operand read as it is used.  Held for the step
+    // the operands spilled at C = 128; M = N = 32768, D = 256: C = 128
+    // 0.82 -> 0.76 ms, C = 256 1.51 -> 0.99 ms (two query tiles, which now
+    // fit in 249 registers); C = 32 and 64 measured 1 - 3 % slower this way.
+    constexpr bool LAZY = DP == 8 && CT >= 8;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);
-      load_k_tile_lds<DP>(kb, kt, j, g, kr[kt]);
+      if constexpr (!LAZY) load_k_tile_lds<DP>(kb, kt, j, g, kr[kt]);
     }
     uint4 vr[CT];
     const uint4* vb = reinterpret_cast<const uint4*>(base + KCH * 1024);
+    if constexpr (LAZY) {
+      const int cl = lds_col(j, g);
+      floatx4 acc[QT][2];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) acc[qt][kt] = cin[kt];
+#pragma unroll
+      for (int dc = 0; dc < DP; ++dc) {
+        const uint4 a0 = kb[(dc * 16 + j) * 4 + cl];
+        const uint4 a1 = kb[((DP + dc) * 16 + j) * 4 + cl];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          acc[qt][0] = mfma_qk<T>(a0, qreg[qt][dc], acc[qt][0]);
+          acc[qt][1] = mfma_qk<T>(a1, qreg[qt][dc], acc[qt][1]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      uint4 b[QT];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        float p[2][4];
+        if constexpr (MODE == 2) {
+          const float be = online_check(qt, acc[qt]);
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) p[kt][r] = __builtin_amdgcn_exp2f(fmaf(acc[qt][kt][r], tau2, be));
+        } else {
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float y = fmaf(acc[qt][kt][r], tau2, bq[qt]);
+              p[kt][r] = SH ? exp2_shifted(y) : exp2_clamped(y);
+            }
+        }
+        b[qt] = pack_tile_pair(p);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) {
+        const uint4 a = vb[(16 * ct + j) * 4 + cl];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) O[qt][ct] = mfma_f16(a, b[qt], O[qt][ct]);
+      }
+      return;
+    }
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) vr[ct] = vb[(16 * ct + j) * 4 + lds_col(j, g)];
     if constexpr (DP == 1 && CT == 1 && MODE != 2) {
