@@ -68,6 +68,11 @@ SHAPES = [
     # D > 128 with 65 - 128 channels: one query tile per wave, three phases
     (150, 333, 256, 128, "f16", "f32", "f32", None, 1.0),
     (111, 290, 180, 100, "bf16", "f16", "f32", None, 1.0),
+    # D > 128 with eight or more value tiles (operands read as used), kernel
+    # values near 1e-18 (the shifted and exact row-maximum forward modes) and
+    # bf16 points with C > 128
+    (120, 300, 256, 128, "f16", "f32", "f32", 0.2, 1.0),
+    (100, 280, 200, 200, "bf16", "f32", "f32", 0.25, 1.0),
 ]
 
 
