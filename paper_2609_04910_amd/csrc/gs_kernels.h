@@ -425,7 +425,7 @@ __device__ __forceinline__ uint4 pack_tile_pair(const float (&p)[2][4]) {
 // each LDS operand read as it is used): several channels at D > 64 where the
 // pass then fits in 256 registers without spills in the key loop (checked
 // per instance: D <= 128 with C <= 128, D <= 256 with C <= 32 or C > 64;
-// D > 128 with C > 32 takes one query tile per wave).  Measured against the
+// D > 128 with C > 64 takes one query tile per wave).  Measured against the
 // plain step for fp16 and bf16, M = N = 32768, forward and full gradient:
 // D = 256, C = 128 10.76 -> 4.65 ms (the plain step with two query tiles
 // reloaded 27 spilled values in every key step; 5.3 ms with one); the plain
