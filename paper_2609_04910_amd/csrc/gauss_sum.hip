@@ -69,7 +69,8 @@ inline Dims dims_of(int64_t D, int64_t C) {
 // CU anyway) one wave per SIMD: a K tile read from LDS then feeds two MFMAs,
 // and a single tile per wave is bound by LDS bandwidth; D > 128 with
 // C > 64 keeps one tile (two spilled 27 values inside the key loop; the
-// single channel keeps two with its operands read as they are used).  The
+// single channel keeps two with its operands read as they are used; at
+// 64 < D <= 128 the single channel, read that way, takes four).  The
 // D > 128 forward with C = 65 - 128 keeps two (one spilled value; 0.83 ms
 // against 1.17 ms with one tile at M = N = 32768).
 // (D > 128 with C > 128: two tiles, the operands read as they are used.)
@@ -90,7 +91,7 @@ constexpr int dq_wpb(int DP) { return DP >= 4 ? 2 * kWavesPerBlock : kWavesPerBl
 constexpr int fwd_wpb(int DP) { return DP >= 4 ? 2 * kWavesPerBlock : kWavesPerBlock; }
 
 constexpr int dq_qt(int DP, int CW) {
-  return DP >= 4 ? (DP == 8 && CW >= 4 ? 1 : 2) : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
+  return DP >= 4 ? (DP == 8 && CW >= 4 ? 1 : DP == 4 && CW == 0 ? 4 : 2) : DP == 2 ? (CW == 0 ? 4 : 2) : CW >= 4 ? 2 : 4;
 }
 
 // Every workgroup of a main kernel covers at most kRowPad query rows (the

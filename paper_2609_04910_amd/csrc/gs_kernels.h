@@ -905,9 +905,11 @@ __global__ __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(2))
   // single-channel gradient fits two query tiles in 244 registers this way
   // (D = 256, C = 1, M = 32768, N = 65536, forward and full gradient: two
   // tiles held 9.27 ms, one tile held 5.86 ms, two tiles read as used
-  // 3.96 ms).  At D <= 128, where nothing spills, reading as used measured
-  // 1 - 3 % slower (SVGD mode).
-  constexpr bool LAZY = (SV || CW == 0) && DP == 8;
+  // 3.96 ms).  At 64 < D <= 128 the single-channel step read this way fits
+  // four query tiles (two held: 4.39 ms, four read as used: 3.77 ms at
+  // D = 128, C = 1, M = N = 65536); the SVGD mode there, where nothing
+  // spills, measured 1 - 3 % slower this way.
+  constexpr bool LAZY = (SV && DP == 8) || (CW == 0 && !SV && DP >= 4);
   // K^T operands read from the RT key tiles by transposing LDS reads (no KS
   // copy of the keys in the stream)
   constexpr bool TR = dq_transposed_keys(std::is_same<T, F16>::value, DP, CW);

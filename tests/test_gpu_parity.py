@@ -73,6 +73,10 @@ SHAPES = [
     # bf16 points with C > 128
     (120, 300, 256, 128, "f16", "f32", "f32", 0.2, 1.0),
     (100, 280, 200, 200, "bf16", "f32", "f32", 0.25, 1.0),
+    # 64 < D <= 128 with a single channel: four query tiles per wave in the
+    # gradient, its operands read as they are used
+    (700, 900, 128, 1, "f16", "f32", "f32", None, 1.0),
+    (333, 555, 90, 1, "bf16", "f16", "f32", None, 1.0),
 ]
 
 
