@@ -77,6 +77,10 @@ SHAPES = [
     # gradient, its operands read as they are used
     (700, 900, 128, 1, "f16", "f32", "f32", None, 1.0),
     (333, 555, 90, 1, "bf16", "f16", "f32", None, 1.0),
+    # 64 < D <= 128 with C > 128: two query tiles per wave in the forward,
+    # its operands read as they are used
+    (200, 300, 128, 256, "f16", "f32", "f32", None, 1.0),
+    (150, 260, 100, 200, "bf16", "f16", "f32", None, 1.0),
 ]
 
 
