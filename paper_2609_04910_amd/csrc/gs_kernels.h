@@ -689,10 +689,11 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
     // the operands spilled at C = 128; M = N = 32768, D = 256: C = 128
     // 0.82 -> 0.76 ms, C = 256 1.51 -> 0.99 ms (two query tiles, which now
     // fit in 249 registers); C = 32 and 64 measured 1 - 3 % slower this way.
-    // 64 < D <= 128 with C > 128: two query tiles instead of one this way
-    // (D = 128, C = 256: 1.17 -> 0.78 ms); at C <= 128 (no spill, two tiles
-    // either way) it measured 3 % slower.
-    constexpr bool LAZY = (DP == 8 && CT >= 8) || (DP == 4 && CT >= 16);
+    // At every D with C > 128: two query tiles instead of one this way
+    // (C = 256, M = N = 32768: D = 128 1.17 -> 0.78 ms, D = 64 1.53 -> 0.70,
+    // D = 32 1.42 -> 0.66); at 64 < D <= 128 with C <= 128 (no spill, two
+    // tiles either way) it measured 3 % slower.
+    constexpr bool LAZY = (DP == 8 && CT >= 8) || CT >= 16;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);

@@ -81,6 +81,10 @@ SHAPES = [
     # its operands read as they are used
     (200, 300, 128, 256, "f16", "f32", "f32", None, 1.0),
     (150, 260, 100, 200, "bf16", "f16", "f32", None, 1.0),
+    # D <= 64 with C > 128 (two query tiles, operands read as used), also in
+    # the shifted and exact row-maximum modes
+    (260, 300, 64, 256, "f16", "f32", "f32", None, 1.0),
+    (130, 170, 20, 150, "bf16", "f16", "f32", 0.5, 1.5),
 ]
 
 
