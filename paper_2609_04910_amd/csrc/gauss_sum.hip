@@ -73,9 +73,10 @@ inline Dims dims_of(int64_t D, int64_t C) {
 // 64 < D <= 128 the single channel, read that way, takes four).  The
 // D > 128 forward with C = 65 - 128 keeps two (one spilled value; 0.83 ms
 // against 1.17 ms with one tile at M = N = 32768).
-// (C > 128: two tiles at every D, the operands read as they are used.)
+// (C > 128: two tiles at every D, and D <= 64 with C = 65 - 128: four,
+// the operands read as they are used.)
 constexpr int fwd_qt(int DP, int CT) {
-  return CT >= 16 ? 2 : CT == 8 ? 2 : (DP == 8 && CT > 1) ? 2 : (DP <= 2 && CT <= 2) ? 8 : 4;
+  return CT >= 16 ? 2 : CT == 8 ? (DP <= 2 ? 4 : 2) : (DP == 8 && CT > 1) ? 2 : (DP <= 2 && CT <= 2) ? 8 : 4;
 }
 // Every workgroup's rows lie inside the padded row range.
 static_assert(kRowPad % (kBlockThreads / 4 * 8) == 0 && kRowPad % 256 == 0, "row padding vs. query tiles");

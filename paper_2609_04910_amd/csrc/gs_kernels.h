@@ -692,8 +692,10 @@ __global__ __launch_bounds__(kWave * WPB) void k_fwd(
     // At every D with C > 128: two query tiles instead of one this way
     // (C = 256, M = N = 32768: D = 128 1.17 -> 0.78 ms, D = 64 1.53 -> 0.70,
     // D = 32 1.42 -> 0.66); at 64 < D <= 128 with C <= 128 (no spill, two
-    // tiles either way) it measured 3 % slower.
-    constexpr bool LAZY = (DP == 8 && CT >= 8) || CT >= 16;
+    // tiles either way) it measured 3 % slower.  D <= 64 with C = 65 - 128
+    // fits four query tiles instead of two this way (C = 128: D = 64
+    // 0.45 -> 0.38 ms, D = 32 0.45 -> 0.34 ms).
+    constexpr bool LAZY = (DP == 8 && CT >= 8) || CT >= 16 || (DP <= 2 && CT == 8);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       cin[kt] = *reinterpret_cast<const floatx4*>(sc + 16 * kt + 4 * g);

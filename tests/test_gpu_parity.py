@@ -85,6 +85,9 @@ SHAPES = [
     # the shifted and exact row-maximum modes
     (260, 300, 64, 256, "f16", "f32", "f32", None, 1.0),
     (130, 170, 20, 150, "bf16", "f16", "f32", 0.5, 1.5),
+    # D <= 64 with C = 65 - 128: four query tiles per wave in the forward
+    (300, 400, 48, 100, "f16", "f32", "f32", None, 1.0),
+    (200, 250, 30, 128, "bf16", "f16", "f32", 0.3, 1.5),
 ]
 
 
